@@ -1,0 +1,178 @@
+/*
+ * packmamba.h -- C ABI of the packed causal conv1d and packed selective scan
+ * (PackMamba, arXiv 2408.03865) on AMD Instinct MI355X (gfx950).
+ *
+ * Packing (§3.1): many variable-length sequences are concatenated along the
+ * sequence axis into rows of length `seqlen`; `position_indices` (batch, seqlen)
+ * int32 holds each token's 0-based position inside its own sequence, so a 0
+ * marks a sequence start.  Neither operator passes information across a start:
+ * the conv drops taps that reach before the start (Alg. 1, §3.3) and the scan
+ * forces its multiplier exp(delta * A) to 0 at the start (Alg. 2, §3.4).
+ *
+ * Conventions shared by every entry point
+ *  - Every pointer is a DEVICE pointer owned by the caller.  The library never
+ *    allocates, frees or synchronises; it only enqueues kernels on `stream`
+ *    (a hipStream_t; NULL means the null stream).  It keeps no mutable global
+ *    state, so concurrent calls on different streams are independent.
+ *  - Layout: contiguous, row-major, sequence axis innermost:
+ *      activations (x, u, delta, z, out, dout and their gradients)  (batch, dim, seqlen)
+ *      B, C, dB, dC                                                 (batch, dstate, seqlen)
+ *      A, dA                                                        (dim, dstate)
+ *      conv weight and dweight                                      (dim, width)
+ *      D, delta_bias, conv bias and their gradients                 (dim)
+ *      position_indices                                             (batch, seqlen)
+ *  - dtype: activation inputs (x, u, delta, z, dout), B and C are float
+ *    (PACKMAMBA_F32) or bfloat16 bits (PACKMAMBA_BF16, PACKMAMBA_BF16_F32OUT).
+ *    Activation outputs (out, dx, du, ddelta, dz) are bfloat16 for
+ *    PACKMAMBA_BF16 and float otherwise.  Parameters, their gradients, dB and dC
+ *    are always float.  Arithmetic and scan state are fp32; bfloat16 outputs
+ *    are rounded once, to nearest even.
+ *  - Every pointer must be 16-byte aligned (PACKMAMBA_ERR_ALIGN otherwise).
+ *  - Argument errors are returned synchronously, before anything is enqueued.
+ *    Faults inside kernels are asynchronous and surface at the caller's next
+ *    synchronisation.  PACKMAMBA_ERR_LAUNCH reports a failed launch.
+ *  - Precondition (not checked on the hot path): position_indices[b,0] == 0 and
+ *    position_indices[b,l] is 0 or position_indices[b,l-1]+1.
+ *    packmamba_check_position_indices() verifies it on demand.
+ */
+#ifndef PACKMAMBA_H
+#define PACKMAMBA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define PACKMAMBA_ABI_VERSION 1
+
+/* dtype codes of the activation tensors */
+#define PACKMAMBA_F32 0            /* fp32 inputs, fp32 outputs */
+#define PACKMAMBA_BF16 1           /* bf16 inputs, bf16 outputs */
+#define PACKMAMBA_BF16_F32OUT 2    /* bf16 inputs, fp32 outputs (same arithmetic as PACKMAMBA_BF16,
+                                      before the final rounding) */
+
+/* Token stride of the scan states saved by the forward for the backward. */
+#define PACKMAMBA_STATE_STRIDE 128
+
+typedef enum {
+    PACKMAMBA_OK = 0,
+    PACKMAMBA_ERR_NULL = 1,         /* required pointer NULL, or a gradient/optional-input pair mismatched */
+    PACKMAMBA_ERR_SHAPE = 2,        /* a dimension <= 0, or sizes overflow */
+    PACKMAMBA_ERR_UNSUPPORTED = 3,  /* dtype, width (2..4) or dstate (16) not supported */
+    PACKMAMBA_ERR_ALIGN = 4,        /* a pointer is not 16-byte aligned */
+    PACKMAMBA_ERR_WORKSPACE = 5,    /* workspace NULL or smaller than the *_workspace_size() result */
+    PACKMAMBA_ERR_LAUNCH = 6        /* the HIP runtime rejected a kernel launch */
+} packmamba_status;
+
+/* ABI version of the loaded library (PACKMAMBA_ABI_VERSION). */
+int packmamba_abi_version(void);
+
+/* Static, NUL-terminated description of a status code. */
+const char* packmamba_status_string(int status);
+
+/*
+ * Causal depthwise conv1d with sequence-start masking, forward (Alg. 1, §3.3).
+ *   pre[b,d,l] = bias[d] + sum_{k=0}^{width-1} [k <= pos[b,l]] * weight[d,width-1-k] * x[b,d,l-k]
+ *   out = silu ? pre * sigmoid(pre) : pre
+ * The tap that reaches k tokens back is used only if it stays inside the output
+ * token's own sequence; weight[d, width-1] multiplies the current token.
+ *   x, out: dtype (batch, dim, seqlen); weight (dim, width); bias (dim) or NULL;
+ *   width in [2, 4].
+ */
+int packmamba_causal_conv1d_fwd(const void* x, const float* weight, const float* bias,
+                                const int32_t* position_indices, void* out,
+                                int64_t batch, int64_t dim, int64_t seqlen, int32_t width,
+                                int32_t dtype, int32_t silu, void* stream);
+
+/* Bytes of workspace packmamba_causal_conv1d_bwd needs. */
+size_t packmamba_causal_conv1d_bwd_workspace_size(int64_t batch, int64_t dim, int64_t seqlen,
+                                                  int32_t width);
+
+/*
+ * Causal conv1d backward (§3.3, §3.5): gradients of sum(dout * out).
+ *   dx[b,d,j] = sum_k [pos[b,j+k] >= k] * weight[d,width-1-k] * g[b,d,j+k]
+ *   (the "reverse indices" of the next width-1 tokens), with g = dout * d out/d pre;
+ *   dweight[d,width-1-k] = sum_{b,l} [k <= pos[b,l]] g[b,d,l] x[b,d,l-k];
+ *   dbias[d] = sum_{b,l} g[b,d,l].
+ *   dx: dtype; dweight (dim, width) and dbias (dim) are overwritten; dbias must
+ *   be NULL iff bias is NULL.  The parameter sums are deterministic (fixed order).
+ */
+int packmamba_causal_conv1d_bwd(const void* x, const float* weight, const float* bias,
+                                const int32_t* position_indices, const void* dout,
+                                void* dx, float* dweight, float* dbias,
+                                void* workspace, size_t workspace_bytes,
+                                int64_t batch, int64_t dim, int64_t seqlen, int32_t width,
+                                int32_t dtype, int32_t silu, void* stream);
+
+/* Bytes of the optional saved-states buffer of packmamba_selective_scan_fwd:
+ * (batch, dim, ceil(seqlen / PACKMAMBA_STATE_STRIDE), dstate) floats. */
+size_t packmamba_selective_scan_fwd_saved_states_size(int64_t batch, int64_t dim, int64_t seqlen,
+                                                      int32_t dstate);
+
+/*
+ * Packed selective scan, forward (Eqs. 1a, 1b, 2a; Alg. 2; §3.4).
+ *   dt[b,d,l]   = softplus(delta[b,d,l] + delta_bias[d])   (softplus if delta_softplus,
+ *                 identity above 20; delta_bias NULL means 0)
+ *   Abar        = pos[b,l] == 0 ? 0 : exp(dt * A[d,n])      (reset at every sequence start)
+ *   h[n]        = Abar * h[n] + dt * B[b,n,l] * u[b,d,l]     (h = 0 at every row start)
+ *   y           = sum_n C[b,n,l] * h[n] + D[d] * u[b,d,l]   (D NULL means 0)
+ *   out[b,d,l]  = z ? y * z * sigmoid(z) : y                 (z NULL means no gate)
+ *   u, delta, z, out: dtype (batch, dim, seqlen); B, C: dtype (batch, dstate, seqlen);
+ *   A (dim, dstate), D (dim), delta_bias (dim): float.  dstate must be 16.
+ *   saved_states: NULL, or a float buffer of
+ *   packmamba_selective_scan_fwd_saved_states_size() bytes that receives h after
+ *   token min((c+1)*PACKMAMBA_STATE_STRIDE, seqlen)-1 for every chunk c, laid out
+ *   (batch, dim, chunk, dstate); the backward reuses it instead of recomputing.
+ *   `out` may be NULL when saved_states is not (states only).
+ */
+int packmamba_selective_scan_fwd(const void* u, const void* delta, const float* A,
+                                 const void* B, const void* C, const float* D, const void* z,
+                                 const float* delta_bias, int32_t delta_softplus,
+                                 const int32_t* position_indices, void* out, float* saved_states,
+                                 int64_t batch, int64_t dim, int64_t seqlen, int32_t dstate,
+                                 int32_t dtype, void* stream);
+
+/* Bytes of workspace packmamba_selective_scan_bwd needs (includes room to
+ * recompute the saved states when the caller passes none). */
+size_t packmamba_selective_scan_bwd_workspace_size(int64_t batch, int64_t dim, int64_t seqlen,
+                                                   int32_t dstate);
+
+/*
+ * Packed selective scan, backward (§3.4): gradients of sum(dout * out) for the
+ * forward above.  The reverse recurrence
+ *   dh_l = Abar_{l+1} * dh_{l+1} + C_l * dy_l,   Abar_{l+1} = 0 where token l+1 starts a sequence,
+ * carries the matching reset; a reset multiplier is the constant 0, so no
+ * gradient flows to delta or A through it.
+ *   Inputs: as the forward, same order, plus dout (dtype) and saved_states
+ *   (NULL: recomputed into the workspace).
+ *   Outputs (overwritten): du, ddelta (dtype, like u); dA (dim, dstate);
+ *   dB, dC (batch, dstate, seqlen) float; dD (dim) iff D != NULL;
+ *   dz (dtype) iff z != NULL; ddelta_bias (dim) iff delta_bias != NULL.
+ *   Sums over channels and tokens use per-block partials in the workspace and a
+ *   second pass in fixed order: results are bitwise reproducible.
+ */
+int packmamba_selective_scan_bwd(const void* u, const void* delta, const float* A,
+                                 const void* B, const void* C, const float* D, const void* z,
+                                 const float* delta_bias, int32_t delta_softplus,
+                                 const int32_t* position_indices, const void* dout,
+                                 const float* saved_states,
+                                 void* du, void* ddelta, float* dA, float* dB, float* dC,
+                                 float* dD, void* dz, float* ddelta_bias,
+                                 void* workspace, size_t workspace_bytes,
+                                 int64_t batch, int64_t dim, int64_t seqlen, int32_t dstate,
+                                 int32_t dtype, void* stream);
+
+/*
+ * Checks the index contract of §3.1 on the device: stores 1 to *d_flag (a device
+ * int32 the caller zeroes beforehand) if any token violates
+ * "pos[b,0] == 0 and pos[b,l] in {0, pos[b,l-1]+1}"; leaves it untouched otherwise.
+ */
+int packmamba_check_position_indices(const int32_t* position_indices, int64_t batch,
+                                     int64_t seqlen, int32_t* d_flag, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* PACKMAMBA_H */

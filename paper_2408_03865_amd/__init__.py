@@ -1,0 +1,144 @@
+"""PackMamba's packed causal conv1d and selective scan on MI355X (gfx950).
+
+Thin torch-facing wrappers over the C ABI of ``libpackmamba.so`` (see
+``include/packmamba.h``).  They allocate outputs and workspace with torch on
+the tensors' device, pass raw pointers and the current stream, and check the
+status.  Nothing is computed here.
+
+    out = causal_conv1d_fwd(x, weight, bias, position_indices, silu=True)
+    dx, dweight, dbias = causal_conv1d_bwd(x, weight, bias, position_indices, dout, silu=True)
+    out, states = selective_scan_fwd(u, delta, A, B, C, D, z, delta_bias, True, position_indices,
+                                     return_states=True)
+    grads = selective_scan_bwd(u, delta, A, B, C, D, z, delta_bias, True, position_indices, dout,
+                               saved_states=states)
+"""
+from __future__ import annotations
+
+from typing import Dict, Optional
+
+from . import _lib
+from ._lib import BF16, BF16_F32OUT, F32, STATE_STRIDE, PackMambaError, load
+
+__all__ = [
+    "causal_conv1d_fwd", "causal_conv1d_bwd", "selective_scan_fwd", "selective_scan_bwd",
+    "check_position_indices", "saved_states_size", "PackMambaError", "load", "F32", "BF16",
+    "STATE_STRIDE", "BF16_F32OUT",
+]
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _code(t, out_f32: bool = False) -> int:
+    torch = _torch()
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16_F32OUT if out_f32 else BF16
+    raise TypeError(f"unsupported activation dtype {t.dtype}")
+
+
+def _empty_out(t, out_f32: bool):
+    torch = _torch()
+    return torch.empty(t.shape, dtype=torch.float32 if out_f32 else t.dtype, device=t.device)
+
+
+def _p(t) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(t) -> int:
+    return _torch().cuda.current_stream(t.device).cuda_stream
+
+
+def _workspace(nbytes: int, device):
+    torch = _torch()
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+
+
+def causal_conv1d_fwd(x, weight, bias, position_indices, silu: bool = True, out_f32: bool = False):
+    """out_f32: for bf16 x, return fp32 outputs (the values before the bf16 rounding)."""
+    Nb, Dn, L = x.shape
+    out = _empty_out(x, out_f32)
+    st = load().packmamba_causal_conv1d_fwd(_p(x), _p(weight), _p(bias), _p(position_indices), _p(out),
+                                            Nb, Dn, L, weight.shape[1], _code(x, out_f32), int(silu),
+                                            _stream(x))
+    _lib.check("packmamba_causal_conv1d_fwd", st)
+    return out
+
+
+def causal_conv1d_bwd(x, weight, bias, position_indices, dout, silu: bool = True, workspace=None,
+                      out_f32: bool = False):
+    torch = _torch()
+    Nb, Dn, L = x.shape
+    W = weight.shape[1]
+    lib = load()
+    dx = _empty_out(x, out_f32)
+    dw = torch.empty_like(weight)
+    db = torch.empty_like(bias) if bias is not None else None
+    need = lib.packmamba_causal_conv1d_bwd_workspace_size(Nb, Dn, L, W)
+    ws = workspace if workspace is not None else _workspace(need, x.device)
+    st = lib.packmamba_causal_conv1d_bwd(_p(x), _p(weight), _p(bias), _p(position_indices), _p(dout),
+                                         _p(dx), _p(dw), _p(db), _p(ws), ws.numel(), Nb, Dn, L, W,
+                                         _code(x, out_f32), int(silu), _stream(x))
+    _lib.check("packmamba_causal_conv1d_bwd", st)
+    return dx, dw, db
+
+
+def saved_states_size(batch: int, dim: int, seqlen: int, dstate: int = 16) -> int:
+    return int(load().packmamba_selective_scan_fwd_saved_states_size(batch, dim, seqlen, dstate))
+
+
+def selective_scan_fwd(u, delta, A, B, C, D, z, delta_bias, delta_softplus, position_indices,
+                       return_states: bool = False, out=True, out_f32: bool = False):
+    torch = _torch()
+    Nb, Dn, L = u.shape
+    N = A.shape[1]
+    o = _empty_out(u, out_f32) if out else None
+    states = None
+    if return_states:
+        nch = (L + STATE_STRIDE - 1) // STATE_STRIDE
+        states = torch.empty((Nb, Dn, nch, N), dtype=torch.float32, device=u.device)
+    st = load().packmamba_selective_scan_fwd(
+        _p(u), _p(delta), _p(A), _p(B), _p(C), _p(D), _p(z), _p(delta_bias), int(delta_softplus),
+        _p(position_indices), _p(o), _p(states), Nb, Dn, L, N, _code(u, out_f32), _stream(u))
+    _lib.check("packmamba_selective_scan_fwd", st)
+    return (o, states) if return_states else o
+
+
+def selective_scan_bwd(u, delta, A, B, C, D, z, delta_bias, delta_softplus, position_indices, dout,
+                       saved_states=None, workspace=None, out_f32: bool = False) -> Dict[str, object]:
+    torch = _torch()
+    Nb, Dn, L = u.shape
+    N = A.shape[1]
+    lib = load()
+    g = {
+        "du": _empty_out(u, out_f32), "ddelta": _empty_out(u, out_f32), "dA": torch.empty_like(A),
+        "dB": torch.empty(B.shape, dtype=torch.float32, device=u.device),
+        "dC": torch.empty(C.shape, dtype=torch.float32, device=u.device),
+        "dD": torch.empty_like(D) if D is not None else None,
+        "dz": _empty_out(z, out_f32) if z is not None else None,
+        "ddelta_bias": torch.empty_like(delta_bias) if delta_bias is not None else None,
+    }
+    need = lib.packmamba_selective_scan_bwd_workspace_size(Nb, Dn, L, N)
+    ws = workspace if workspace is not None else _workspace(need, u.device)
+    st = lib.packmamba_selective_scan_bwd(
+        _p(u), _p(delta), _p(A), _p(B), _p(C), _p(D), _p(z), _p(delta_bias), int(delta_softplus),
+        _p(position_indices), _p(dout), _p(saved_states), _p(g["du"]), _p(g["ddelta"]), _p(g["dA"]),
+        _p(g["dB"]), _p(g["dC"]), _p(g["dD"]), _p(g["dz"]), _p(g["ddelta_bias"]), _p(ws), ws.numel(),
+        Nb, Dn, L, N, _code(u, out_f32), _stream(u))
+    _lib.check("packmamba_selective_scan_bwd", st)
+    return g
+
+
+def check_position_indices(position_indices) -> bool:
+    """True if the indices satisfy the packing contract (checked on the device)."""
+    torch = _torch()
+    flag = torch.zeros(4, dtype=torch.int32, device=position_indices.device)
+    Nb, L = position_indices.shape
+    st = load().packmamba_check_position_indices(_p(position_indices), Nb, L, _p(flag),
+                                                 _stream(position_indices))
+    _lib.check("packmamba_check_position_indices", st)
+    return int(flag[0].item()) == 0

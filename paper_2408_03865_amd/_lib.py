@@ -1,0 +1,79 @@
+"""ctypes binding of libpackmamba.so: the C ABI in include/packmamba.h, same names.
+
+Argument marshalling only.  Every step of the path runs in the HIP kernels of
+the library; torch provides device memory and the current stream.  There is no
+fallback: if the library is missing or was not built for this GPU, loading
+raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libpackmamba.so")
+
+F32, BF16, BF16_F32OUT = 0, 1, 2
+STATE_STRIDE = 128
+ABI_VERSION = 1
+
+STATUS = {0: "OK", 1: "ERR_NULL", 2: "ERR_SHAPE", 3: "ERR_UNSUPPORTED", 4: "ERR_ALIGN",
+          5: "ERR_WORKSPACE", 6: "ERR_LAUNCH"}
+
+# Every symbol the header declares.
+EXPORTS = (
+    "packmamba_abi_version", "packmamba_status_string",
+    "packmamba_causal_conv1d_fwd", "packmamba_causal_conv1d_bwd_workspace_size",
+    "packmamba_causal_conv1d_bwd", "packmamba_selective_scan_fwd_saved_states_size",
+    "packmamba_selective_scan_fwd", "packmamba_selective_scan_bwd_workspace_size",
+    "packmamba_selective_scan_bwd", "packmamba_check_position_indices",
+)
+
+
+class PackMambaError(RuntimeError):
+    def __init__(self, fn: str, status: int, text: str):
+        super().__init__(f"{fn}: {STATUS.get(status, status)} ({text})")
+        self.status = status
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load the HIP library (raises if it is absent: build with paper_2408_03865_amd/build.py)."""
+    global _lib
+    if _lib is not None and path == LIB_PATH:
+        return _lib
+    if not os.path.exists(path):
+        raise FileNotFoundError(f"{path} is missing; build it with `python paper_2408_03865_amd/build.py`")
+    lib = ctypes.CDLL(path)
+    vp, i64, i32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
+    lib.packmamba_abi_version.restype = ctypes.c_int
+    lib.packmamba_status_string.argtypes = [ctypes.c_int]
+    lib.packmamba_status_string.restype = ctypes.c_char_p
+    lib.packmamba_causal_conv1d_fwd.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, i32, i32, i32, vp]
+    lib.packmamba_causal_conv1d_bwd_workspace_size.argtypes = [i64, i64, i64, i32]
+    lib.packmamba_causal_conv1d_bwd_workspace_size.restype = sz
+    lib.packmamba_causal_conv1d_bwd.argtypes = [vp] * 9 + [sz, i64, i64, i64, i32, i32, i32, vp]
+    lib.packmamba_selective_scan_fwd_saved_states_size.argtypes = [i64, i64, i64, i32]
+    lib.packmamba_selective_scan_fwd_saved_states_size.restype = sz
+    lib.packmamba_selective_scan_fwd.argtypes = [vp] * 8 + [i32, vp, vp, vp, i64, i64, i64, i32, i32, vp]
+    lib.packmamba_selective_scan_bwd_workspace_size.argtypes = [i64, i64, i64, i32]
+    lib.packmamba_selective_scan_bwd_workspace_size.restype = sz
+    lib.packmamba_selective_scan_bwd.argtypes = ([vp] * 8 + [i32] + [vp] * 12 + [sz, i64, i64, i64, i32, i32, vp])
+    lib.packmamba_check_position_indices.argtypes = [vp, i64, i64, vp, vp]
+    for name in ("packmamba_causal_conv1d_fwd", "packmamba_causal_conv1d_bwd",
+                 "packmamba_selective_scan_fwd", "packmamba_selective_scan_bwd",
+                 "packmamba_check_position_indices"):
+        getattr(lib, name).restype = ctypes.c_int
+    if lib.packmamba_abi_version() != ABI_VERSION:
+        raise RuntimeError("libpackmamba ABI version mismatch")
+    if path == LIB_PATH:
+        _lib = lib
+    return lib
+
+
+def check(fn: str, status: int) -> None:
+    if status != 0:
+        text = load().packmamba_status_string(status).decode()
+        raise PackMambaError(fn, status, text)

@@ -1,0 +1,150 @@
+// common.hpp -- device helpers shared by the gfx950 kernels: storage types,
+// vector loads/stores with ragged tails, and DPP lane moves for wave64 rows.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace pm {
+
+// ---------------------------------------------------------------------------
+// storage types: float, or bf16 held as its 16-bit pattern
+// ---------------------------------------------------------------------------
+struct bf16_t {
+    uint16_t bits;
+};
+
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// two floats -> two bf16 packed in one word, round to nearest even (v_cvt_pk_bf16_f32)
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+    f32x2 v = {a, b};
+    bf16x2 r = __builtin_convertvector(v, bf16x2);
+    return __builtin_bit_cast(uint32_t, r);
+}
+
+template <typename T> struct Storage;
+
+template <> struct Storage<float> {
+    static constexpr int kBytes = 4;
+    static constexpr int kPerVec = 4;     // elements per 16-byte vector
+    __device__ static float load1(const float* p) { return *p; }
+    __device__ static void store1(float* p, float v) { *p = v; }
+    __device__ static void unpack(const u32x4& w, float* v) {
+        v[0] = __uint_as_float(w.x); v[1] = __uint_as_float(w.y);
+        v[2] = __uint_as_float(w.z); v[3] = __uint_as_float(w.w);
+    }
+    __device__ static u32x4 pack(const float* v) {
+        u32x4 w = {__float_as_uint(v[0]), __float_as_uint(v[1]), __float_as_uint(v[2]),
+                   __float_as_uint(v[3])};
+        return w;
+    }
+};
+
+template <> struct Storage<bf16_t> {
+    static constexpr int kBytes = 2;
+    static constexpr int kPerVec = 8;
+    __device__ static float load1(const bf16_t* p) { return __uint_as_float((uint32_t)p->bits << 16); }
+    __device__ static void store1(bf16_t* p, float v) {
+        p->bits = (uint16_t)(pack_bf16x2(v, 0.0f) & 0xffffu);
+    }
+    __device__ static void unpack(const u32x4& w, float* v) {
+        v[0] = bf16_lo(w.x); v[1] = bf16_hi(w.x); v[2] = bf16_lo(w.y); v[3] = bf16_hi(w.y);
+        v[4] = bf16_lo(w.z); v[5] = bf16_hi(w.z); v[6] = bf16_lo(w.w); v[7] = bf16_hi(w.w);
+    }
+    __device__ static u32x4 pack(const float* v) {
+        u32x4 w = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]),
+                   pack_bf16x2(v[6], v[7])};
+        return w;
+    }
+};
+
+// Load K consecutive elements starting at row[l0] (K a multiple of the vector width),
+// converting to float; elements at or beyond L read as `fill`.  `vec` says the row
+// base is 16-byte aligned and L is a multiple of the vector width.
+template <typename T, int K>
+__device__ __forceinline__ void load_run(const T* __restrict__ row, int64_t l0, int64_t L, bool vec,
+                                         float* v, float fill = 0.0f) {
+    constexpr int PV = Storage<T>::kPerVec;
+    static_assert(K % PV == 0, "K must be a multiple of the vector width");
+    if (vec && l0 + K <= L) {
+#pragma unroll
+        for (int i = 0; i < K / PV; ++i) {
+            const u32x4 w = *reinterpret_cast<const u32x4*>(row + l0 + i * PV);
+            Storage<T>::unpack(w, v + i * PV);
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < K; ++i) v[i] = (l0 + i < L) ? Storage<T>::load1(row + l0 + i) : fill;
+    }
+}
+
+// Store K consecutive elements (rounding to T) at row[l0]; elements beyond L are dropped.
+template <typename T, int K>
+__device__ __forceinline__ void store_run(T* __restrict__ row, int64_t l0, int64_t L, bool vec,
+                                          const float* v) {
+    constexpr int PV = Storage<T>::kPerVec;
+    if (vec && l0 + K <= L) {
+#pragma unroll
+        for (int i = 0; i < K / PV; ++i)
+            *reinterpret_cast<u32x4*>(row + l0 + i * PV) = Storage<T>::pack(v + i * PV);
+    } else {
+#pragma unroll
+        for (int i = 0; i < K; ++i)
+            if (l0 + i < L) Storage<T>::store1(row + l0 + i, v[i]);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// DPP lane moves inside 16-lane rows (bound_ctrl off: a lane whose source is
+// outside its row keeps `old`)
+// ---------------------------------------------------------------------------
+enum : int {
+    kRowShl1 = 0x101,
+    kRowShr1 = 0x111,
+    kNewBcast0 = 0x150,
+    kNewBcast15 = 0x15f,
+};
+__host__ __device__ constexpr int row_shl(int n) { return 0x100 + n; }
+__host__ __device__ constexpr int row_shr(int n) { return 0x110 + n; }
+
+template <int CTRL>
+__device__ __forceinline__ float dpp(float old, float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, old),
+                                                                  __builtin_bit_cast(int, v), CTRL,
+                                                                  0xf, 0xf, false));
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
+__device__ __forceinline__ float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+// ln(1 + x) for x >= 0, accurate for small x: ln(u) * x / (u - 1) with u = 1 + x,
+// the rounding error of u cancelling between numerator and denominator
+// (D. Goldberg, "What every computer scientist should know about floating-point
+// arithmetic", 1991, Theorem 4).
+__device__ __forceinline__ float log1p_f(float x) {
+    const float u = 1.0f + x;
+    const float d = u - 1.0f;
+    return d == 0.0f ? x : kLn2 * fast_log2(u) * (x * fast_rcp(d));
+}
+
+// softplus with the identity above 20
+__device__ __forceinline__ float softplus_f(float s) {
+    return s > 20.0f ? s : log1p_f(fast_exp2(s * kLog2e));
+}
+__device__ __forceinline__ float sigmoid_f(float v) { return fast_rcp(1.0f + fast_exp2(-v * kLog2e)); }
+
+// Flat wave lane id and the lane's position inside its 16-lane row.
+__device__ __forceinline__ int lane_id() { return (int)(threadIdx.x & 63); }
+
+}  // namespace pm

@@ -1,0 +1,246 @@
+// conv1d.hip -- packed causal depthwise conv1d, forward and backward (Alg. 1, §3.3, §3.5).
+//
+// HBM-bound streaming kernels.  One 256-thread block per (batch, channel) row;
+// each thread owns 8 consecutive tokens per step (one 16-byte vector of bf16,
+// two of fp32) and loops along the row.  The width-1 halo comes from the
+// neighbouring vector, which the neighbouring lane loads in the same instruction,
+// so it is served by the cache and costs no extra HBM traffic.  The tap mask
+// uses only integer compares against the token's position index, read with the
+// same coalesced vector loads (§3.5): the forward keeps the tap reaching k tokens
+// back iff k <= pos[l]; the backward's dx reads the next width-1 tokens'
+// indices ("reverse indices") and keeps tap k iff pos[j+k] >= k.
+#include "common.hpp"
+#include "launch.hpp"
+
+namespace pm {
+namespace {
+
+constexpr int kTok = 8;        // tokens per thread per step
+constexpr int kThreads = 256;
+
+__device__ __forceinline__ void load_pos(const int32_t* __restrict__ pr, int64_t l0, int64_t L,
+                                         bool pvec, int* p) {
+    if (pvec && l0 + kTok <= L) {
+        const u32x4 a = *reinterpret_cast<const u32x4*>(pr + l0);
+        const u32x4 b = *reinterpret_cast<const u32x4*>(pr + l0 + 4);
+        p[0] = (int)a.x; p[1] = (int)a.y; p[2] = (int)a.z; p[3] = (int)a.w;
+        p[4] = (int)b.x; p[5] = (int)b.y; p[6] = (int)b.z; p[7] = (int)b.w;
+    } else {
+#pragma unroll
+        for (int i = 0; i < kTok; ++i) p[i] = (l0 + i < L) ? pr[l0 + i] : 0;
+    }
+}
+
+// pre-activation of the token at index i of `xs`, where xs[kTok + t] holds token
+// l0 + t and xs[kTok - 1 - t] holds token l0 - 1 - t
+template <int W>
+__device__ __forceinline__ float conv_pre(const float* xs, int i, int p, const float* wk, float b0) {
+    float acc = b0;
+#pragma unroll
+    for (int k = 0; k < W; ++k)
+        if (k <= p) acc = fmaf(wk[W - 1 - k], xs[kTok + i - k], acc);
+    return acc;
+}
+
+template <typename T, typename TO, int W>
+__global__ __launch_bounds__(kThreads) void conv1d_fwd_kernel(
+    const T* __restrict__ x, const float* __restrict__ w, const float* __restrict__ bias,
+    const int32_t* __restrict__ pos, TO* __restrict__ out, int64_t dim, int64_t L, int silu,
+    int vec, int pvec) {
+    const int64_t row = blockIdx.x;
+    const int64_t b = row / dim, d = row - b * dim;
+    const T* xr = x + row * L;
+    TO* orow = out + row * L;
+    const int32_t* pr = pos + b * L;
+    float wk[W];
+#pragma unroll
+    for (int k = 0; k < W; ++k) wk[k] = w[d * W + k];
+    const float b0 = bias ? bias[d] : 0.0f;
+
+    for (int64_t l0 = (int64_t)threadIdx.x * kTok; l0 < L; l0 += (int64_t)kThreads * kTok) {
+        float xs[2 * kTok];
+        load_run<T, kTok>(xr, l0, L, vec, xs + kTok);
+        if (l0 > 0) load_run<T, kTok>(xr, l0 - kTok, L, vec, xs);
+        else {
+#pragma unroll
+            for (int i = 0; i < kTok; ++i) xs[i] = 0.0f;
+        }
+        int p[kTok];
+        load_pos(pr, l0, L, pvec, p);
+        float o[kTok];
+#pragma unroll
+        for (int i = 0; i < kTok; ++i) {
+            const float v = conv_pre<W>(xs, i, p[i], wk, b0);
+            o[i] = silu ? v * sigmoid_f(v) : v;
+        }
+        store_run<TO, kTok>(orow, l0, L, vec, o);
+    }
+}
+
+// Block-wide sum of NV values per thread; thread 0 receives the totals.
+template <int NV>
+__device__ __forceinline__ void block_sum(float* v, float* lds /* NV * (kThreads/64) */) {
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) v[j] += __shfl_xor(v[j], off, 64);
+    }
+    const int wave = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) {
+#pragma unroll
+        for (int j = 0; j < NV; ++j) lds[j * (kThreads / 64) + wave] = v[j];
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+#pragma unroll
+        for (int j = 0; j < NV; ++j) {
+            float s = 0.0f;
+            for (int q = 0; q < kThreads / 64; ++q) s += lds[j * (kThreads / 64) + q];
+            v[j] = s;
+        }
+    }
+}
+
+template <typename T, typename TO, int W>
+__global__ __launch_bounds__(kThreads) void conv1d_bwd_kernel(
+    const T* __restrict__ x, const float* __restrict__ w, const float* __restrict__ bias,
+    const int32_t* __restrict__ pos, const T* __restrict__ dout, TO* __restrict__ dx,
+    float* __restrict__ partial, int64_t dim, int64_t L, int silu, int vec, int pvec) {
+    __shared__ float red[(W + 1) * (kThreads / 64)];
+    const int64_t row = blockIdx.x;
+    const int64_t b = row / dim, d = row - b * dim;
+    const T* xr = x + row * L;
+    const T* gr = dout + row * L;
+    TO* dxr = dx + row * L;
+    const int32_t* pr = pos + b * L;
+    float wk[W];
+#pragma unroll
+    for (int k = 0; k < W; ++k) wk[k] = w[d * W + k];
+    const float b0 = bias ? bias[d] : 0.0f;
+    float acc[W + 1];   // dw[0..W-1], dbias
+#pragma unroll
+    for (int j = 0; j <= W; ++j) acc[j] = 0.0f;
+
+    for (int64_t l0 = (int64_t)threadIdx.x * kTok; l0 < L; l0 += (int64_t)kThreads * kTok) {
+        // x for tokens l0-8 .. l0+15 (pre-activations of this vector and the next W-1 tokens)
+        float xs[3 * kTok];
+        if (l0 > 0) load_run<T, kTok>(xr, l0 - kTok, L, vec, xs);
+        else {
+#pragma unroll
+            for (int i = 0; i < kTok; ++i) xs[i] = 0.0f;
+        }
+        load_run<T, kTok>(xr, l0, L, vec, xs + kTok);
+        load_run<T, kTok>(xr, l0 + kTok, L, vec, xs + 2 * kTok);
+        float gs[2 * kTok];
+        load_run<T, kTok>(gr, l0, L, vec, gs);
+        load_run<T, kTok>(gr, l0 + kTok, L, vec, gs + kTok);
+        int p[2 * kTok];
+        load_pos(pr, l0, L, pvec, p);
+        load_pos(pr, l0 + kTok, L, pvec, p + kTok);
+        // g = dout * d out / d pre for tokens l0 .. l0+kTok+W-2 (zero beyond L: dout reads 0)
+        float g[kTok + W - 1];
+#pragma unroll
+        for (int t = 0; t < kTok + W - 1; ++t) {
+            float gt = gs[t];
+            if (silu) {
+                const float v = conv_pre<W>(xs, t, p[t], wk, b0);
+                const float s = sigmoid_f(v);
+                gt *= s * (1.0f + v * (1.0f - s));
+            }
+            g[t] = gt;
+        }
+        // dx through the reverse indices: tap k of token j+k is live iff pos[j+k] >= k
+        float o[kTok];
+#pragma unroll
+        for (int i = 0; i < kTok; ++i) {
+            float a = 0.0f;
+#pragma unroll
+            for (int k = 0; k < W; ++k)
+                if (p[i + k] >= k) a = fmaf(wk[W - 1 - k], g[i + k], a);
+            o[i] = a;
+        }
+        store_run<TO, kTok>(dxr, l0, L, vec, o);
+        // parameter gradients from this thread's own tokens
+#pragma unroll
+        for (int i = 0; i < kTok; ++i) {
+#pragma unroll
+            for (int k = 0; k < W; ++k)
+                if (k <= p[i]) acc[W - 1 - k] = fmaf(g[i], xs[kTok + i - k], acc[W - 1 - k]);
+            acc[W] += g[i];
+        }
+    }
+    block_sum<W + 1>(acc, red);
+    if (threadIdx.x == 0) {
+#pragma unroll
+        for (int j = 0; j <= W; ++j) partial[row * (W + 1) + j] = acc[j];
+    }
+}
+
+// dw[d,k] = sum_b partial[b,d,k]; dbias[d] = sum_b partial[b,d,W]  (fixed order over b)
+__global__ void conv1d_bwd_finalize(const float* __restrict__ partial, float* __restrict__ dw,
+                                    float* __restrict__ dbias, int64_t batch, int64_t dim, int W) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= dim * (W + 1)) return;
+    const int64_t d = i / (W + 1);
+    const int j = (int)(i - d * (W + 1));
+    float s = 0.0f;
+    for (int64_t b = 0; b < batch; ++b) s += partial[(b * dim + d) * (W + 1) + j];
+    if (j < W) dw[d * W + j] = s;
+    else if (dbias) dbias[d] = s;
+}
+
+template <typename T, typename TO>
+hipError_t conv_fwd_t(const ConvArgs& a, hipStream_t s) {
+    const int vec = (a.seqlen % Storage<T>::kPerVec) == 0 && (a.seqlen % Storage<TO>::kPerVec) == 0;
+    const int pvec = (a.seqlen % 4) == 0;
+    dim3 grid((unsigned)(a.batch * a.dim)), block(kThreads);
+    const T* x = static_cast<const T*>(a.x);
+    TO* o = static_cast<TO*>(a.out);
+    switch (a.width) {
+        case 2: hipLaunchKernelGGL((conv1d_fwd_kernel<T, TO, 2>), grid, block, 0, s, x, a.w, a.bias, a.pos, o, a.dim, a.seqlen, a.silu, vec, pvec); break;
+        case 3: hipLaunchKernelGGL((conv1d_fwd_kernel<T, TO, 3>), grid, block, 0, s, x, a.w, a.bias, a.pos, o, a.dim, a.seqlen, a.silu, vec, pvec); break;
+        default: hipLaunchKernelGGL((conv1d_fwd_kernel<T, TO, 4>), grid, block, 0, s, x, a.w, a.bias, a.pos, o, a.dim, a.seqlen, a.silu, vec, pvec); break;
+    }
+    return hipGetLastError();
+}
+
+template <typename T, typename TO>
+hipError_t conv_bwd_t(const ConvArgs& a, hipStream_t s) {
+    const int vec = (a.seqlen % Storage<T>::kPerVec) == 0 && (a.seqlen % Storage<TO>::kPerVec) == 0;
+    const int pvec = (a.seqlen % 4) == 0;
+    dim3 grid((unsigned)(a.batch * a.dim)), block(kThreads);
+    const T* x = static_cast<const T*>(a.x);
+    const T* g = static_cast<const T*>(a.dout);
+    TO* dx = static_cast<TO*>(a.out);
+    switch (a.width) {
+        case 2: hipLaunchKernelGGL((conv1d_bwd_kernel<T, TO, 2>), grid, block, 0, s, x, a.w, a.bias, a.pos, g, dx, a.partial, a.dim, a.seqlen, a.silu, vec, pvec); break;
+        case 3: hipLaunchKernelGGL((conv1d_bwd_kernel<T, TO, 3>), grid, block, 0, s, x, a.w, a.bias, a.pos, g, dx, a.partial, a.dim, a.seqlen, a.silu, vec, pvec); break;
+        default: hipLaunchKernelGGL((conv1d_bwd_kernel<T, TO, 4>), grid, block, 0, s, x, a.w, a.bias, a.pos, g, dx, a.partial, a.dim, a.seqlen, a.silu, vec, pvec); break;
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int64_t n = a.dim * (a.width + 1);
+    hipLaunchKernelGGL(conv1d_bwd_finalize, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,
+                       a.partial, a.dw, a.dbias, a.batch, a.dim, (int)a.width);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_conv1d_fwd(const ConvArgs& a, hipStream_t s) {
+    switch (a.dtype) {
+        case 1: return conv_fwd_t<bf16_t, bf16_t>(a, s);
+        case 2: return conv_fwd_t<bf16_t, float>(a, s);
+        default: return conv_fwd_t<float, float>(a, s);
+    }
+}
+
+hipError_t launch_conv1d_bwd(const ConvArgs& a, hipStream_t s) {
+    switch (a.dtype) {
+        case 1: return conv_bwd_t<bf16_t, bf16_t>(a, s);
+        case 2: return conv_bwd_t<bf16_t, float>(a, s);
+        default: return conv_bwd_t<float, float>(a, s);
+    }
+}
+
+}  // namespace pm

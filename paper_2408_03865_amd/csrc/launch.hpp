@@ -1,0 +1,66 @@
+// launch.hpp -- host-side launchers of the gfx950 kernels, called by the C ABI
+// after argument validation.  Each returns hipSuccess or the launch error.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace pm {
+
+struct ConvArgs {
+    const void* x;
+    const float* w;
+    const float* bias;
+    const int32_t* pos;
+    const void* dout;   // bwd only
+    void* out;          // fwd: out; bwd: dx
+    float* dw;          // bwd only
+    float* dbias;       // bwd only
+    float* partial;     // bwd only: (batch*dim, width+1)
+    int64_t batch, dim, seqlen;
+    int32_t width, dtype, silu;
+};
+
+hipError_t launch_conv1d_fwd(const ConvArgs& a, hipStream_t s);
+hipError_t launch_conv1d_bwd(const ConvArgs& a, hipStream_t s);
+
+struct ScanArgs {
+    const void* u;
+    const void* delta;
+    const float* A;
+    const void* B;
+    const void* C;
+    const float* D;
+    const void* z;
+    const float* delta_bias;
+    const int32_t* pos;
+    int32_t softplus;
+    // forward
+    void* out;
+    float* states;          // (batch, dim, nchunk, dstate); written by fwd, read by bwd
+    // backward
+    const void* dout;
+    void* du;
+    void* ddelta;
+    void* dz;
+    float* dA;
+    float* dB;
+    float* dC;
+    float* dD;
+    float* ddelta_bias;
+    float* part_bc;         // (batch, groups, 2, dstate, seqlen)
+    float* part_chan;       // (batch, dim, dstate + 2)
+    int64_t batch, dim, seqlen;
+    int32_t dstate, dtype;
+};
+
+// channels reduced on chip per dB/dC partial in the backward
+constexpr int kScanBwdChannels = 16;
+
+hipError_t launch_scan_fwd(const ScanArgs& a, hipStream_t s);
+hipError_t launch_scan_bwd(const ScanArgs& a, hipStream_t s);
+hipError_t launch_check_pos(const int32_t* pos, int64_t batch, int64_t seqlen, int32_t* flag,
+                            hipStream_t s);
+
+}  // namespace pm

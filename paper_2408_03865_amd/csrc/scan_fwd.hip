@@ -1,0 +1,230 @@
+// scan_fwd.hip -- packed selective scan, forward (Eqs. 1a, 1b, 2a; Alg. 2; §3.4).
+//
+// Layout of the work (gfx950, wave64):
+//  - a block is 4 waves = 16 rows of 16 lanes; each 16-lane DPP row owns one
+//    channel d of one batch row b, so a block covers 16 channels of one b;
+//  - each lane owns K consecutive tokens, a row owns a chunk of 16*K tokens, and
+//    the block walks the sequence chunk by chunk, carrying the state h[n] of
+//    every channel from one chunk to the next in registers;
+//  - B and C of the chunk (shared by the 16 channels) and the reset mask derived
+//    from the position indices are staged once per chunk in LDS as fp32 with a
+//    padded layout (conflict-free 16-byte reads), read from HBM with coalesced
+//    vector loads (§3.5);
+//  - per state n the pair (Abar, Bbar x) = (exp(dt*A), dt*B*u) is folded over the
+//    lane's K tokens, the 16 lane aggregates are combined by an inclusive DPP
+//    scan inside the row, the chunk carry is applied, and the lane replays its K
+//    tokens from its start state to form h and y += C h.
+//  - Reset (Alg. 2): Abar = exp2(dt * A*log2e + M) with M = -inf on a token whose
+//    position index is 0, so the multiplier is exactly 0 there at no extra cost;
+//    a product range that contains a start is therefore 0 inside the fold and the
+//    scan alike (§3.4).
+//  - Tokens past the row end get dt = 0 and u = 0, i.e. the identity (1, 0).
+#include "common.hpp"
+#include "launch.hpp"
+
+namespace pm {
+namespace {
+
+constexpr int kN = 16;              // d_state
+constexpr int kRows = 16;           // channels per block
+constexpr int kThreads = 256;
+constexpr int kStride = 128;        // saved-state token stride (PACKMAMBA_STATE_STRIDE)
+
+template <int K>
+struct FwdSmem {
+    static constexpr int kSeg = K + 4;                 // padded floats per lane segment
+    float B[kN][16][kSeg];
+    float C[kN][16][kSeg];
+    float M[16][kSeg];
+};
+
+struct FwdParams {
+    const void* u;
+    const void* delta;
+    const float* A;
+    const void* B;
+    const void* C;
+    const float* D;
+    const void* z;
+    const float* delta_bias;
+    const int32_t* pos;
+    void* out;
+    float* states;
+    int64_t dim, L;
+    int nchunk_states;
+    int softplus;
+    int vec;
+};
+
+// inclusive scan of the affine maps h -> P h + H across the 16 lanes of a row
+__device__ __forceinline__ void row_scan_fwd(float& P, float& H) {
+#define PM_STEP(n)                                              \
+    {                                                           \
+        const float Hp = dpp<row_shr(n)>(0.0f, H);              \
+        const float Pp = dpp<row_shr(n)>(1.0f, P);              \
+        H = fmaf(P, Hp, H);                                     \
+        P = P * Pp;                                             \
+    }
+    PM_STEP(1) PM_STEP(2) PM_STEP(4) PM_STEP(8)
+#undef PM_STEP
+}
+
+template <typename T, typename TO, int K>
+__global__ __launch_bounds__(kThreads) void scan_fwd_kernel(FwdParams p) {
+    constexpr int CH = 16 * K;
+    constexpr int PV = Storage<T>::kPerVec;
+    using Smem = FwdSmem<K>;
+    __shared__ Smem sm;
+
+    const int tid = threadIdx.x;
+    const int j = tid & 15;                       // lane position inside the row
+    const int r = tid >> 4;                       // row (channel) inside the block
+    const int64_t b = blockIdx.y;
+    const int64_t d_raw = (int64_t)blockIdx.x * kRows + r;
+    const bool active = d_raw < p.dim;
+    const int64_t d = active ? d_raw : p.dim - 1;
+    const int64_t L = p.L;
+    const int64_t rowoff = (b * p.dim + d) * L;
+
+    const T* ur = static_cast<const T*>(p.u) + rowoff;
+    const T* dr = static_cast<const T*>(p.delta) + rowoff;
+    const T* zr = p.z ? static_cast<const T*>(p.z) + rowoff : nullptr;
+    TO* orow = p.out ? static_cast<TO*>(p.out) + rowoff : nullptr;
+    const T* Bb = static_cast<const T*>(p.B) + b * kN * L;
+    const T* Cb = static_cast<const T*>(p.C) + b * kN * L;
+    const int32_t* pr = p.pos + b * L;
+
+    float A2[kN], carry[kN];
+#pragma unroll
+    for (int n = 0; n < kN; ++n) {
+        A2[n] = p.A[d * kN + n] * kLog2e;
+        carry[n] = 0.0f;
+    }
+    const float Dd = p.D ? p.D[d] : 0.0f;
+    const float dbias = p.delta_bias ? p.delta_bias[d] : 0.0f;
+
+    const int64_t nchunk = (L + CH - 1) / CH;
+    for (int64_t c = 0; c < nchunk; ++c) {
+        const int64_t lb = c * CH;
+        // ---- stage B, C and the reset mask of this chunk in LDS ----
+        for (int idx = tid * PV; idx < kN * CH; idx += kThreads * PV) {
+            const int n = idx / CH, t = idx - n * CH;
+            float vb[PV], vc[PV];
+            load_run<T, PV>(Bb + (int64_t)n * L, lb + t, L, p.vec, vb);
+            load_run<T, PV>(Cb + (int64_t)n * L, lb + t, L, p.vec, vc);
+            float* db = &sm.B[n][t / K][t % K];
+            float* dc = &sm.C[n][t / K][t % K];
+#pragma unroll
+            for (int i = 0; i < PV; ++i) { db[i] = vb[i]; dc[i] = vc[i]; }
+        }
+        for (int t = tid; t < CH; t += kThreads) {
+            const int64_t l = lb + t;
+            sm.M[t / K][t % K] = (l < L && pr[l] == 0) ? -INFINITY : 0.0f;
+        }
+        __syncthreads();
+
+        // ---- per-token inputs of this lane ----
+        const int64_t l0 = lb + (int64_t)j * K;
+        float dt[K], du[K], y[K], M[K];
+        {
+            float uv[K];
+            load_run<T, K>(ur, l0, L, p.vec, uv);
+            load_run<T, K>(dr, l0, L, p.vec, dt);
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                const float s = dt[k] + dbias;
+                float v = p.softplus ? softplus_f(s) : s;
+                v = (l0 + k < L) ? v : 0.0f;       // identity past the row end
+                dt[k] = v;
+                du[k] = v * uv[k];
+                y[k] = Dd * uv[k];
+            }
+#pragma unroll
+            for (int k = 0; k < K; k += 4) {
+                const f32x4 m = *reinterpret_cast<const f32x4*>(&sm.M[j][k]);
+                M[k] = m.x; M[k + 1] = m.y; M[k + 2] = m.z; M[k + 3] = m.w;
+            }
+        }
+
+        // ---- states ----
+#pragma unroll 1
+        for (int n = 0; n < kN; ++n) {
+            float a[K], bx[K];
+#pragma unroll
+            for (int k = 0; k < K; k += 4) {
+                const f32x4 bv = *reinterpret_cast<const f32x4*>(&sm.B[n][j][k]);
+                const float bb[4] = {bv.x, bv.y, bv.z, bv.w};
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    a[k + q] = fast_exp2(fmaf(dt[k + q], A2[n], M[k + q]));
+                    bx[k + q] = du[k + q] * bb[q];
+                }
+            }
+            // fold the lane's K tokens into one affine map h -> P h + H
+            float P = a[0], H = bx[0];
+#pragma unroll
+            for (int k = 1; k < K; ++k) {
+                H = fmaf(a[k], H, bx[k]);
+                P = P * a[k];
+            }
+            row_scan_fwd(P, H);
+            const float hend = fmaf(P, carry[n], H);          // state after this lane's last token
+            float h = dpp<kRowShr1>(carry[n], hend);          // state before this lane's first token
+            carry[n] = dpp<kNewBcast15>(0.0f, hend);          // state after the chunk
+#pragma unroll
+            for (int k = 0; k < K; k += 4) {
+                const f32x4 cv = *reinterpret_cast<const f32x4*>(&sm.C[n][j][k]);
+                const float cc[4] = {cv.x, cv.y, cv.z, cv.w};
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    h = fmaf(a[k + q], h, bx[k + q]);
+                    y[k + q] = fmaf(cc[q], h, y[k + q]);
+                }
+            }
+            // saved states: h after every kStride-th token
+            if (p.states && active && (((j + 1) * K) % kStride) == 0) {
+                const int64_t sc = (l0 + K) / kStride - 1;
+                if (sc < p.nchunk_states)
+                    p.states[((b * p.dim + d) * p.nchunk_states + sc) * kN + n] = hend;
+            }
+        }
+
+        // ---- gate and store ----
+        if (orow && active) {
+            if (zr) {
+                float zv[K];
+                load_run<T, K>(zr, l0, L, p.vec, zv);
+#pragma unroll
+                for (int k = 0; k < K; ++k) y[k] = y[k] * zv[k] * sigmoid_f(zv[k]);
+            }
+            store_run<TO, K>(orow, l0, L, p.vec, y);
+        }
+        __syncthreads();      // LDS is restaged for the next chunk
+    }
+}
+
+template <typename T, typename TO, int K>
+hipError_t launch_t(const ScanArgs& a, hipStream_t s) {
+    FwdParams p;
+    p.u = a.u; p.delta = a.delta; p.A = a.A; p.B = a.B; p.C = a.C; p.D = a.D; p.z = a.z;
+    p.delta_bias = a.delta_bias; p.pos = a.pos; p.out = a.out; p.states = a.states;
+    p.dim = a.dim; p.L = a.seqlen;
+    p.nchunk_states = (int)((a.seqlen + kStride - 1) / kStride);
+    p.softplus = a.softplus;
+    p.vec = (a.seqlen % Storage<T>::kPerVec) == 0 && (a.seqlen % Storage<TO>::kPerVec) == 0;
+    dim3 grid((unsigned)((a.dim + kRows - 1) / kRows), (unsigned)a.batch);
+    hipLaunchKernelGGL((scan_fwd_kernel<T, TO, K>), grid, dim3(kThreads), 0, s, p);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_scan_fwd(const ScanArgs& a, hipStream_t s) {
+    switch (a.dtype) {
+        case 1: return launch_t<bf16_t, bf16_t, 16>(a, s);
+        case 2: return launch_t<bf16_t, float, 16>(a, s);
+        default: return launch_t<float, float, 16>(a, s);
+    }
+}
+
+}  // namespace pm

@@ -1,0 +1,100 @@
+"""The C-ABI library on the CPU: it loads, exports every declared symbol, and rejects bad
+arguments before anything is enqueued (no GPU needed; skipped where a GPU is visible so
+that fake pointers can never reach a kernel)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "packmamba.h")
+
+
+def _lib():
+    from paper_2408_03865_amd import _lib as L
+    if not os.path.exists(L.LIB_PATH):
+        import __graft_entry__
+        __graft_entry__.build()
+    return L.load()
+
+
+def test_exports_every_declared_symbol():
+    from paper_2408_03865_amd import _lib as L
+    names = set(re.findall(r"\b(packmamba_\w+)\s*\(", open(HEADER).read()))
+    assert names == set(L.EXPORTS), names ^ set(L.EXPORTS)
+    lib = _lib()
+    for n in names:
+        assert hasattr(lib, n), n
+    assert lib.packmamba_abi_version() == 1
+
+
+def test_status_strings():
+    lib = _lib()
+    for s in range(7):
+        assert lib.packmamba_status_string(s)
+    assert b"unknown" in lib.packmamba_status_string(99)
+
+
+def test_sizes():
+    lib = _lib()
+    assert lib.packmamba_selective_scan_fwd_saved_states_size(8, 4096, 4096, 16) == 8 * 4096 * 32 * 16 * 4
+    assert lib.packmamba_selective_scan_fwd_saved_states_size(1, 1, 129, 16) == 2 * 16 * 4
+    assert lib.packmamba_selective_scan_fwd_saved_states_size(1, 1, 129, 8) == 0
+    assert lib.packmamba_causal_conv1d_bwd_workspace_size(2, 3, 5, 4) >= 2 * 3 * 5 * 4
+    assert lib.packmamba_causal_conv1d_bwd_workspace_size(2, 3, 5, 5) == 0
+    assert lib.packmamba_selective_scan_bwd_workspace_size(8, 4096, 4096, 16) > 0
+    assert lib.packmamba_selective_scan_bwd_workspace_size(0, 4096, 4096, 16) == 0
+
+
+def _gpu_visible():
+    try:
+        import torch
+        return torch.cuda.is_available()
+    except Exception:
+        return False
+
+
+@pytest.mark.skipif(_gpu_visible(), reason="fake pointers are only passed where no GPU exists")
+def test_argument_errors_before_launch():
+    lib = _lib()
+    P = 0x10000          # fake, aligned; every case below must fail validation first
+    U = 0x10008          # fake, misaligned
+    conv = lib.packmamba_causal_conv1d_fwd
+    assert conv(None, P, None, P, P, 1, 1, 8, 4, 0, 1, None) == 1           # x NULL
+    assert conv(P, P, None, P, P, 0, 1, 8, 4, 0, 1, None) == 2              # batch 0
+    assert conv(P, P, None, P, P, 1, 1, -3, 4, 0, 1, None) == 2             # seqlen < 0
+    assert conv(P, P, None, P, P, 1, 1, 1 << 40, 4, 0, 1, None) == 2        # too large
+    assert conv(P, P, None, P, P, 1, 1, 8, 5, 0, 1, None) == 3              # width 5
+    assert conv(P, P, None, P, P, 1, 1, 8, 1, 0, 1, None) == 3              # width 1
+    assert conv(P, P, None, P, P, 1, 1, 8, 4, 7, 1, None) == 3              # dtype
+    assert conv(U, P, None, P, P, 1, 1, 8, 4, 0, 1, None) == 4              # misaligned x
+    cbwd = lib.packmamba_causal_conv1d_bwd
+    assert cbwd(P, P, P, P, P, P, P, None, P, 1 << 20, 1, 1, 8, 4, 0, 1, None) == 1   # bias without dbias
+    assert cbwd(P, P, None, P, P, P, P, None, P, 1, 1, 1, 8, 4, 0, 1, None) == 5      # workspace small
+    assert cbwd(P, P, None, P, P, P, P, None, None, 1 << 20, 1, 1, 8, 4, 0, 1, None) == 5
+    fwd = lib.packmamba_selective_scan_fwd
+    args = [P, P, P, P, P, None, None, None, 1, P, P, None, 1, 1, 8, 16, 1, None]
+    a = list(args); a[0] = None
+    assert fwd(*a) == 1
+    a = list(args); a[10] = None                                            # no out and no states
+    assert fwd(*a) == 1
+    a = list(args); a[15] = 8                                               # dstate 8
+    assert fwd(*a) == 3
+    a = list(args); a[6] = U                                                # misaligned z
+    assert fwd(*a) == 4
+    a = list(args); a[12] = 70000                                           # batch too large
+    assert fwd(*a) == 2
+    bwd = lib.packmamba_selective_scan_bwd
+    bargs = [P, P, P, P, P, P, None, None, 1, P, P, None, P, P, P, P, P, P, None, None, P, 1 << 40,
+             1, 1, 8, 16, 1, None]
+    a = list(bargs); a[17] = None                                           # D without dD
+    assert bwd(*a) == 1
+    a = list(bargs); a[18] = P                                              # dz without z
+    assert bwd(*a) == 1
+    a = list(bargs); a[21] = 16                                             # workspace too small
+    assert bwd(*a) == 5
+    a = list(bargs); a[25] = 32
+    assert bwd(*a) == 3
+    assert lib.packmamba_check_position_indices(None, 1, 8, P, None) == 1
+    assert lib.packmamba_check_position_indices(U, 1, 8, P, None) == 4

@@ -1,0 +1,87 @@
+"""GPU edge cases against the oracle: ragged shapes, optional inputs absent, other widths,
+general parameter values, and the device index check."""
+import numpy as np
+import pytest
+
+import workloads as W
+from gpu_common import PER_B, PER_CHANNEL, PER_TOKEN, TOL, compare, gpu_inputs, i32, note, oracle_run, run_gpu
+
+pytestmark = pytest.mark.gpu
+
+ALL = PER_TOKEN + PER_CHANNEL + PER_B
+
+SHAPES = [(1, 1, 1), (1, 1, 7), (2, 17, 129), (1, 40, 300), (3, 5, 1000), (1, 16, 256), (2, 33, 2049),
+          (1, 3, 4104)]
+
+
+def _cfg(batch, dim, seqlen, dtype, width=4):
+    return W.Config("edge", "edge", batch, seqlen, dim, 16, width, dtype,
+                    ("lognormal", 2.0, 1.5, 1, max(seqlen, 1)), 7000 + batch * 131 + dim * 7 + seqlen)
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "x".join(map(str, s)))
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_ragged_shapes(shape, dtype):
+    cfg = _cfg(*shape, dtype)
+    note(f"edge shape {shape} {dtype}")
+    d = W.make_inputs(cfg, variant="general")
+    g = gpu_inputs(d, dtype)
+    r = run_gpu(g, out_f32=(dtype == "bf16"))
+    compare(r, oracle_run(d), TOL[dtype], ALL, label=f"{shape} {dtype} ")
+
+
+OPTIONS = {
+    "no-D": dict(D=None),
+    "no-z": dict(z=None),
+    "no-delta_bias": dict(delta_bias=None),
+    "no-softplus": dict(softplus=False),
+    "no-conv-bias": dict(bias=None),
+    "no-silu": dict(silu=False),
+    "bare": dict(D=None, z=None, delta_bias=None, softplus=False, bias=None, silu=False),
+}
+
+
+@pytest.mark.parametrize("name", list(OPTIONS))
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_optional_inputs(name, dtype):
+    cfg = _cfg(2, 24, 600, dtype)
+    note(f"edge options {name} {dtype}")
+    d = W.make_inputs(cfg, variant="general")
+    if name in ("no-softplus", "bare"):
+        # without softplus the step is delta + delta_bias itself: keep it positive
+        d["delta"] = np.abs(d["delta"]) * 0.5 + 0.05
+        d["delta_bias"] = np.abs(d["delta_bias"]) * 0.01
+        if dtype == "bf16":
+            d["delta"] = W.bf16_round(d["delta"])
+    g = gpu_inputs(d, dtype)
+    opts = OPTIONS[name]
+    gopts = {k: (None if v is None else v) for k, v in opts.items()}
+    r = run_gpu(g, out_f32=(dtype == "bf16"), opts=gopts)
+    compare(r, oracle_run(d, opts=opts), TOL[dtype], ALL, label=f"{name} {dtype} ")
+
+
+@pytest.mark.parametrize("width", [2, 3])
+def test_other_widths(width):
+    cfg = _cfg(2, 20, 515, "f32", width=width)
+    d = W.make_inputs(cfg, variant="general")
+    r = run_gpu(gpu_inputs(d, "f32"))
+    compare(r, oracle_run(d), TOL["f32"], ("conv_out", "dx", "dw", "dbias"), label=f"width {width} ")
+
+
+def test_paper_variant_long_sequences_f32():
+    """A = -(n+1), the configs' recipe, on long sequences in fp32."""
+    cfg = W.config("1", dtype="f32", dim=32, batch=2)
+    d = W.make_inputs(cfg)
+    r = run_gpu(gpu_inputs(d, "f32"))
+    compare(r, oracle_run(d), TOL["f32"], ALL, label="paper f32 ")
+
+
+def test_check_position_indices():
+    import paper_2408_03865_amd as P
+    good = W.positions_from_lengths([[3, 1, 4, 1, 7], [16]], 16)
+    assert P.check_position_indices(i32(good))
+    for b, l, v in [(0, 0, 1), (1, 5, 9), (0, 4, 2), (0, 15, 0)]:
+        bad = good.copy()
+        bad[b, l] = v
+        import oracle
+        assert P.check_position_indices(i32(bad)) == (oracle.check_positions(bad) == -1), (b, l, v)
