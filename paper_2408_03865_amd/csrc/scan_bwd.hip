@@ -27,15 +27,18 @@ constexpr int kRows = 16;
 constexpr int kThreads = 256;
 constexpr int kK = 8;               // tokens per lane
 constexpr int kCH = 16 * kK;        // tokens per chunk == saved-state stride
-constexpr int kSeg = kK + 4;        // padded floats per lane segment in LDS
 static_assert(kCH == 128, "chunk must equal the saved-state stride");
 static_assert(kRows == kScanBwdChannels, "partials are per 16 channels");
 
-struct BwdSmem {
-    float B[kN][16][kSeg];
-    float C[kN][16][kSeg];
-    float M[16][kSeg];
+struct __attribute__((aligned(16))) BwdSmem {
+    float B[kN][16][kK];            // [state][lane][token]
+    float C[kN][16][kK];
+    float M[16][kK];                // 0, or -inf on a sequence start
     float red[2][2][kRows][kCH];    // [state parity][dB|dC][row][token]
+    float A2[kRows][kN];            // A * log2(e)
+    float xc[kRows][kN];            // dh at the first token of the chunk to the right
+    float an[kRows][kN];            // Abar at the first token of the chunk to the right
+    float dA[kRows][kN];            // per-channel dA accumulators
 };
 
 struct BwdParams {
@@ -62,17 +65,12 @@ struct BwdParams {
     int vec;
 };
 
-template <int S>
-__device__ __forceinline__ void scan_step(float& P, float& H) {
-    // combine with the lane S positions away (row_shr: earlier lanes; row_shl: later)
-    const float Hp = dpp<S>(0.0f, H);
-    const float Pp = dpp<S>(1.0f, P);
-    H = fmaf(P, Hp, H);
-    P = P * Pp;
-}
-
+// Three waves per SIMD (at most 168 VGPRs): three blocks share a CU, so one block's
+// barrier waits are covered by the other two; measured faster than two waves
+// without any spill.
 template <typename T, typename TO>
-__global__ __launch_bounds__(kThreads) void scan_bwd_kernel(BwdParams p) {
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3, 3)))
+void scan_bwd_kernel(BwdParams p) {
     constexpr int PV = Storage<T>::kPerVec;
     constexpr int K = kK;
     __shared__ BwdSmem sm;
@@ -100,21 +98,23 @@ __global__ __launch_bounds__(kThreads) void scan_bwd_kernel(BwdParams p) {
     const int32_t* pr = p.pos + b * L;
     const float* st = p.states + (b * p.dim + d) * (int64_t)p.nchunk_states * kN;
 
-    float A2[kN], xcarry[kN], anext[kN], dAacc[kN];
-#pragma unroll
-    for (int n = 0; n < kN; ++n) {
-        A2[n] = p.A[d * kN + n] * kLog2e;
-        xcarry[n] = 0.0f;     // dh at the first token of the chunk to the right
-        anext[n] = 0.0f;      // Abar at the first token of the chunk to the right
-        dAacc[n] = 0.0f;
+    {   // per-channel tables
+        const int rr = tid >> 4, n = tid & 15;
+        const int64_t dd = min((int64_t)g * kRows + rr, p.dim - 1);
+        sm.A2[rr][n] = p.A[dd * kN + n] * kLog2e;
+        sm.xc[rr][n] = 0.0f;
+        sm.an[rr][n] = 0.0f;
+        sm.dA[rr][n] = 0.0f;
     }
     const float Dd = p.D ? p.D[d] : 0.0f;
     const float dbias = p.delta_bias ? p.delta_bias[d] : 0.0f;
     float dDacc = 0.0f, dbacc = 0.0f;
+    float dt_next = 0.0f, m_next = 0.0f;     // step and mask of the first token of the chunk to the right
 
     const int64_t nchunk = (L + kCH - 1) / kCH;
     for (int64_t c = nchunk - 1; c >= 0; --c) {
         const int64_t lb = c * kCH;
+        // ---- stage B, C, the reset mask and the chunk-start states in LDS ----
         for (int idx = tid * PV; idx < kN * kCH; idx += kThreads * PV) {
             const int n = idx / kCH, t = idx - n * kCH;
             float vb[PV], vc[PV];
@@ -130,64 +130,73 @@ __global__ __launch_bounds__(kThreads) void scan_bwd_kernel(BwdParams p) {
             sm.M[t / K][t % K] = (l < L && pr[l] == 0) ? -INFINITY : 0.0f;
         }
         __syncthreads();
+        // state at the chunk start (h after token lb-1), saved by the forward
+        const float* hin_src = c > 0 ? st + (c - 1) * kN : nullptr;
 
         // ---- per-token inputs ----
         const int64_t l0 = lb + (int64_t)j * K;
-        float uv[K], dt[K], dlu[K], dyD[K], gsp[K], M[K], yacc[K], sdhB[K], sdA[K];
+        float dt[K], dlu[K], dyD[K], yacc[K], sdhB[K], sdA[K];
+        float S = 0.0f, Mf = 0.0f, Mr = 0.0f, m0 = 0.0f;
         {
-            float dl[K];
+            float dl[K], uv[K];
             load_run<T, K>(ur, l0, L, p.vec, uv);
             load_run<T, K>(dr, l0, L, p.vec, dl);
             load_run<T, K>(gr, l0, L, p.vec, dyD);     // dout for now
+            if (zr) {
+                float zv[K];
+                load_run<T, K>(zr, l0, L, p.vec, zv);
+#pragma unroll
+                for (int k = 0; k < K; ++k) dyD[k] *= zv[k] * sigmoid_f(zv[k]);   // dy = dout * SiLU(z)
+            }
 #pragma unroll
             for (int k = 0; k < K; ++k) {
                 const float s = dl[k] + dbias;
-                float v = s;
-                float gs = 1.0f;
-                if (p.softplus) {
-                    v = softplus_f(s);
-                    gs = s > 20.0f ? 1.0f : sigmoid_f(s);
-                }
-                v = (l0 + k < L) ? v : 0.0f;
+                float v = p.softplus ? softplus_f(s) : s;
+                v = (l0 + k < L) ? v : 0.0f;          // identity past the row end
                 dt[k] = v;
-                gsp[k] = gs;
-                dlu[k] = v * uv[k];
+                if (!active) dyD[k] = 0.0f;           // padding rows contribute nothing to dB, dC
+                dlu[k] = active ? v * uv[k] : 0.0f;
                 yacc[k] = Dd * uv[k];
                 sdhB[k] = 0.0f;
                 sdA[k] = 0.0f;
             }
+            // Lane products of Abar as one exp2 each: prod_k exp2(dt_k A2) = exp2(A2 sum_k dt_k),
+            // forced to 0 when a reset falls inside the product range.
+#pragma unroll
+            for (int k = 0; k < K; k += 4) {
+                const f32x4 m = *reinterpret_cast<const f32x4*>(&sm.M[j][k]);
+                const float mm[4] = {m.x, m.y, m.z, m.w};
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    S += dt[k + q];
+                    Mf += mm[q];
+                    if (k + q > 0) Mr += mm[q];
+                }
+                if (k == 0) m0 = mm[0];
+            }
+        }
+        const float dt0n = dpp<kRowShl1>(dt_next, dt[0]);    // next token's step, across the lane edge
+        const float m0n = dpp<kRowShl1>(m_next, m0);
+        const float Sr = S - dt[0] + dt0n;
+        Mr += m0n;
+        dt_next = dpp<kNewBcast0>(0.0f, dt[0]);
+        m_next = dpp<kNewBcast0>(0.0f, m0);
+        float hin_next = hin_src ? hin_src[0] : 0.0f;
+
+#pragma unroll 1
+        for (int n = 0; n < kN; ++n) {
+            const float A2n = sm.A2[r][n];
+            const float hin = hin_next;
+            if (hin_src && n + 1 < kN) hin_next = hin_src[n + 1];     // prefetch one state ahead
+            const float xc = sm.xc[r][n];
+            const float an = sm.an[r][n];
+            float a[K], ah[K], bv[K], cdy[K], bx[K], M[K];
 #pragma unroll
             for (int k = 0; k < K; k += 4) {
                 const f32x4 m = *reinterpret_cast<const f32x4*>(&sm.M[j][k]);
                 M[k] = m.x; M[k + 1] = m.y; M[k + 2] = m.z; M[k + 3] = m.w;
             }
-        }
-        float zv[K];
-        if (zr) {
-            load_run<T, K>(zr, l0, L, p.vec, zv);
-#pragma unroll
-            for (int k = 0; k < K; ++k) dyD[k] *= zv[k] * sigmoid_f(zv[k]);   // dy = dout * SiLU(z)
-        }
-
-        // saved state at the chunk start (h after token lb-1)
-        float hin[kN];
-        if (c > 0) {
-#pragma unroll
-            for (int n = 0; n < kN; n += 4) {
-                const f32x4 v = *reinterpret_cast<const f32x4*>(st + (c - 1) * kN + n);
-                hin[n] = v.x; hin[n + 1] = v.y; hin[n + 2] = v.z; hin[n + 3] = v.w;
-            }
-        } else {
-#pragma unroll
-            for (int n = 0; n < kN; ++n) hin[n] = 0.0f;
-        }
-
-#pragma unroll 1
-        for (int n = 0; n < kN; ++n) {
-            float a[K], ah[K], bv[K], cdy[K];
-            float dBp[K], dCp[K];
             // ---- replay the forward inside the chunk ----
-            float bx[K];
 #pragma unroll
             for (int k = 0; k < K; k += 4) {
                 const f32x4 v = *reinterpret_cast<const f32x4*>(&sm.B[n][j][k]);
@@ -195,21 +204,16 @@ __global__ __launch_bounds__(kThreads) void scan_bwd_kernel(BwdParams p) {
             }
 #pragma unroll
             for (int k = 0; k < K; ++k) {
-                a[k] = fast_exp2(fmaf(dt[k], A2[n], M[k]));
+                a[k] = fast_exp2(fmaf(dt[k], A2n, M[k]));
                 bx[k] = dlu[k] * bv[k];
             }
-            float P = a[0], H = bx[0];
+            float H = bx[0];
 #pragma unroll
-            for (int k = 1; k < K; ++k) {
-                H = fmaf(a[k], H, bx[k]);
-                P = P * a[k];
-            }
-            scan_step<row_shr(1)>(P, H);
-            scan_step<row_shr(2)>(P, H);
-            scan_step<row_shr(4)>(P, H);
-            scan_step<row_shr(8)>(P, H);
-            const float hend = fmaf(P, hin[n], H);
-            float hprev = dpp<kRowShr1>(hin[n], hend);
+            for (int k = 1; k < K; ++k) H = fmaf(a[k], H, bx[k]);
+            float P = fast_exp2(fmaf(S, A2n, Mf));
+            row_scan_up(P, H);
+            const float hend = fmaf(P, hin, H);
+            float hprev = dpp<kRowShr1>(hin, hend);
 #pragma unroll
             for (int k = 0; k < K; k += 4) {
                 const f32x4 cv = *reinterpret_cast<const f32x4*>(&sm.C[n][j][k]);
@@ -220,52 +224,45 @@ __global__ __launch_bounds__(kThreads) void scan_bwd_kernel(BwdParams p) {
                     ah[kk] = a[kk] * hprev;
                     const float h = ah[kk] + bx[kk];
                     yacc[kk] = fmaf(cc[q], h, yacc[kk]);
-                    dCp[kk] = dyD[kk] * h;
+                    bx[kk] = dyD[kk] * h;                    // dC contribution (reuses bx)
                     cdy[kk] = cc[q] * dyD[kk];
                     hprev = h;
                 }
             }
-            // ---- reverse recurrence ----
-            // multiplier linking token k to k+1: a[k+1]; for the lane's last token it
-            // is the next lane's a[0], or the next chunk's first token on lane 15
-            const float alast = dpp<kRowShl1>(anext[n], a[0]);
-            float Pr = alast, Hr = cdy[K - 1];
+            // ---- reverse recurrence: dh_l = Abar_{l+1} dh_{l+1} + C_l dy_l ----
+            const float alast = dpp<kRowShl1>(an, a[0]);        // Abar of the next lane's first token
+            float Hr = cdy[K - 1];
 #pragma unroll
-            for (int k = K - 2; k >= 0; --k) {
-                Hr = fmaf(a[k + 1], Hr, cdy[k]);
-                Pr = Pr * a[k + 1];
+            for (int k = K - 2; k >= 0; --k) Hr = fmaf(a[k + 1], Hr, cdy[k]);
+            float Pr = fast_exp2(fmaf(Sr, A2n, Mr));
+            row_scan_down(Pr, Hr);
+            const float dhfirst = fmaf(Pr, xc, Hr);            // dh at this lane's first token
+            float dh = dpp<kRowShl1>(xc, dhfirst);               // dh at the next lane's first token
+            if (j == 0) {
+                sm.xc[r][n] = dhfirst;
+                sm.an[r][n] = a[0];
             }
-            scan_step<row_shl(1)>(Pr, Hr);
-            scan_step<row_shl(2)>(Pr, Hr);
-            scan_step<row_shl(4)>(Pr, Hr);
-            scan_step<row_shl(8)>(Pr, Hr);
-            const float dhfirst = fmaf(Pr, xcarry[n], Hr);      // dh at this lane's first token
-            float dh = dpp<kRowShl1>(xcarry[n], dhfirst);       // dh at the next lane's first token
-            xcarry[n] = dpp<kNewBcast0>(0.0f, dhfirst);
-            anext[n] = dpp<kNewBcast0>(0.0f, a[0]);
             float dAl = 0.0f;
+            float dBp[K];
 #pragma unroll
             for (int k = K - 1; k >= 0; --k) {
                 const float am = (k == K - 1) ? alast : a[k + 1];
                 dh = fmaf(am, dh, cdy[k]);
                 sdhB[k] = fmaf(dh, bv[k], sdhB[k]);
                 const float q = dh * ah[k];
-                sdA[k] = fmaf(q, A2[n], sdA[k]);
+                sdA[k] = fmaf(q, A2n, sdA[k]);
                 dAl = fmaf(q, dt[k], dAl);
                 dBp[k] = dh * dlu[k];
             }
-            dAacc[n] += dAl;
+            dAl = row_sum_to_15(dAl);
+            if (j == 15) sm.dA[r][n] += dAl;
             // ---- dB, dC: sum over the block's 16 channels ----
             float* rb = &sm.red[n & 1][0][r][j * K];
             float* rc = &sm.red[n & 1][1][r][j * K];
-            const bool live = active;
 #pragma unroll
             for (int k = 0; k < K; k += 4) {
-                f32x4 vb = {dBp[k], dBp[k + 1], dBp[k + 2], dBp[k + 3]};
-                f32x4 vc = {dCp[k], dCp[k + 1], dCp[k + 2], dCp[k + 3]};
-                if (!live) { vb = f32x4{0.f, 0.f, 0.f, 0.f}; vc = vb; }
-                *reinterpret_cast<f32x4*>(rb + k) = vb;
-                *reinterpret_cast<f32x4*>(rc + k) = vc;
+                *reinterpret_cast<f32x4*>(rb + k) = f32x4{dBp[k], dBp[k + 1], dBp[k + 2], dBp[k + 3]};
+                *reinterpret_cast<f32x4*>(rc + k) = f32x4{bx[k], bx[k + 1], bx[k + 2], bx[k + 3]};
             }
             __syncthreads();
             {
@@ -278,59 +275,57 @@ __global__ __launch_bounds__(kThreads) void scan_bwd_kernel(BwdParams p) {
                 if (l < L)
                     p.part_bc[(((b * p.groups + g) * 2 + which) * kN + n) * L + l] = s;
             }
+            // no second barrier: the next state writes the other buffer, and this one is
+            // rewritten only after every thread has passed the next state's barrier
         }
 
         // ---- per-token gradients ----
-        float o_du[K], o_dd[K], o_dz[K];
-#pragma unroll
-        for (int k = 0; k < K; ++k) {
-            o_du[k] = fmaf(dyD[k], Dd, dt[k] * sdhB[k]);
-            const float ddt = fmaf(uv[k], sdhB[k], sdA[k] * kLn2);   // sdA was built with A*log2e
-            o_dd[k] = ddt * gsp[k];
-            dDacc = fmaf(dyD[k], uv[k], dDacc);
-            dbacc += (l0 + k < L) ? o_dd[k] : 0.0f;
-        }
-        if (zr) {
-            float gv[K];
-            load_run<T, K>(gr, l0, L, p.vec, gv);
+        float o_du[K], o_dd[K];
+        {
+            float dl[K], uv[K];
+            load_run<T, K>(dr, l0, L, p.vec, dl);
+            load_run<T, K>(ur, l0, L, p.vec, uv);
 #pragma unroll
             for (int k = 0; k < K; ++k) {
-                const float sz = sigmoid_f(zv[k]);
-                o_dz[k] = gv[k] * yacc[k] * sz * (1.0f + zv[k] * (1.0f - sz));
+                o_du[k] = fmaf(dyD[k], Dd, dt[k] * sdhB[k]);
+                const float ddt = fmaf(uv[k], sdhB[k], sdA[k] * kLn2);   // sdA was built with A*log2e
+                const float s = dl[k] + dbias;
+                const float gs = p.softplus ? (s > 20.0f ? 1.0f : sigmoid_f(s)) : 1.0f;
+                o_dd[k] = ddt * gs;
+                dDacc = fmaf(dyD[k], uv[k], dDacc);
+                dbacc += (l0 + k < L) ? o_dd[k] : 0.0f;
             }
         }
         if (active) {
             store_run<TO, K>(dur, l0, L, p.vec, o_du);
             store_run<TO, K>(ddr, l0, L, p.vec, o_dd);
-            if (dzr) store_run<TO, K>(dzr, l0, L, p.vec, o_dz);
+            if (dzr) {
+                float zv[K], gv[K], o_dz[K];
+                load_run<T, K>(zr, l0, L, p.vec, zv);
+                load_run<T, K>(gr, l0, L, p.vec, gv);
+#pragma unroll
+                for (int k = 0; k < K; ++k) {
+                    const float sz = sigmoid_f(zv[k]);
+                    o_dz[k] = gv[k] * yacc[k] * sz * (1.0f + zv[k] * (1.0f - sz));
+                }
+                store_run<TO, K>(dzr, l0, L, p.vec, o_dz);
+            }
         }
         __syncthreads();     // LDS is restaged for the next chunk
     }
 
-    // ---- per-channel partials: sum the 16 lanes of the row ----
-#pragma unroll
-    for (int n = 0; n < kN; ++n) {
-        float v = dAacc[n];
-        v += dpp<row_shr(1)>(0.0f, v);
-        v += dpp<row_shr(2)>(0.0f, v);
-        v += dpp<row_shr(4)>(0.0f, v);
-        v += dpp<row_shr(8)>(0.0f, v);
-        dAacc[n] = v;
-    }
-    dDacc += dpp<row_shr(1)>(0.0f, dDacc);
-    dDacc += dpp<row_shr(2)>(0.0f, dDacc);
-    dDacc += dpp<row_shr(4)>(0.0f, dDacc);
-    dDacc += dpp<row_shr(8)>(0.0f, dDacc);
-    dbacc += dpp<row_shr(1)>(0.0f, dbacc);
-    dbacc += dpp<row_shr(2)>(0.0f, dbacc);
-    dbacc += dpp<row_shr(4)>(0.0f, dbacc);
-    dbacc += dpp<row_shr(8)>(0.0f, dbacc);
+    // ---- per-channel partials ----
+    dDacc = row_sum_to_15(dDacc);
+    dbacc = row_sum_to_15(dbacc);
     if (active && j == 15) {
         float* pc = p.part_chan + (b * p.dim + d) * (kN + 2);
-#pragma unroll
-        for (int n = 0; n < kN; ++n) pc[n] = dAacc[n];
         pc[kN] = dDacc;
         pc[kN + 1] = dbacc;
+    }
+    {
+        const int rr = tid >> 4, n = tid & 15;
+        if ((int64_t)g * kRows + rr < p.dim)
+            p.part_chan[(b * p.dim + g * kRows + rr) * (kN + 2) + n] = sm.dA[rr][n];
     }
 }
 

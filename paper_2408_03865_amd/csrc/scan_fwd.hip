@@ -31,11 +31,12 @@ constexpr int kThreads = 256;
 constexpr int kStride = 128;        // saved-state token stride (PACKMAMBA_STATE_STRIDE)
 
 template <int K>
-struct FwdSmem {
-    static constexpr int kSeg = K + 4;                 // padded floats per lane segment
-    float B[kN][16][kSeg];
-    float C[kN][16][kSeg];
-    float M[16][kSeg];
+struct __attribute__((aligned(16))) FwdSmem {
+    float B[kN][16][K];         // [state][lane][token]
+    float C[kN][16][K];
+    float M[16][K];             // 0, or -inf on a sequence start
+    float A2[kRows][kN];        // A * log2(e)
+    float carry[kRows][kN];     // state after the previous chunk
 };
 
 struct FwdParams {
@@ -55,19 +56,6 @@ struct FwdParams {
     int softplus;
     int vec;
 };
-
-// inclusive scan of the affine maps h -> P h + H across the 16 lanes of a row
-__device__ __forceinline__ void row_scan_fwd(float& P, float& H) {
-#define PM_STEP(n)                                              \
-    {                                                           \
-        const float Hp = dpp<row_shr(n)>(0.0f, H);              \
-        const float Pp = dpp<row_shr(n)>(1.0f, P);              \
-        H = fmaf(P, Hp, H);                                     \
-        P = P * Pp;                                             \
-    }
-    PM_STEP(1) PM_STEP(2) PM_STEP(4) PM_STEP(8)
-#undef PM_STEP
-}
 
 template <typename T, typename TO, int K>
 __global__ __launch_bounds__(kThreads) void scan_fwd_kernel(FwdParams p) {
@@ -94,11 +82,11 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_kernel(FwdParams p) {
     const T* Cb = static_cast<const T*>(p.C) + b * kN * L;
     const int32_t* pr = p.pos + b * L;
 
-    float A2[kN], carry[kN];
-#pragma unroll
-    for (int n = 0; n < kN; ++n) {
-        A2[n] = p.A[d * kN + n] * kLog2e;
-        carry[n] = 0.0f;
+    {
+        const int rr = tid >> 4, n = tid & 15;
+        const int64_t dd = min((int64_t)blockIdx.x * kRows + rr, p.dim - 1);
+        sm.A2[rr][n] = p.A[dd * kN + n] * kLog2e;
+        sm.carry[rr][n] = 0.0f;
     }
     const float Dd = p.D ? p.D[d] : 0.0f;
     const float dbias = p.delta_bias ? p.delta_bias[d] : 0.0f;
@@ -115,7 +103,7 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_kernel(FwdParams p) {
             float* db = &sm.B[n][t / K][t % K];
             float* dc = &sm.C[n][t / K][t % K];
 #pragma unroll
-            for (int i = 0; i < PV; ++i) { db[i] = vb[i]; dc[i] = vc[i]; }
+            for (int q = 0; q < PV; ++q) { db[q] = vb[q]; dc[q] = vc[q]; }
         }
         for (int t = tid; t < CH; t += kThreads) {
             const int64_t l = lb + t;
@@ -145,10 +133,16 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_kernel(FwdParams p) {
                 M[k] = m.x; M[k + 1] = m.y; M[k + 2] = m.z; M[k + 3] = m.w;
             }
         }
+        // product of the lane's multipliers as one exp2 (0 if the lane holds a start)
+        float S = 0.0f, Mf = 0.0f;
+#pragma unroll
+        for (int k = 0; k < K; ++k) { S += dt[k]; Mf += M[k]; }
 
         // ---- states ----
 #pragma unroll 1
         for (int n = 0; n < kN; ++n) {
+            const float A2n = sm.A2[r][n];
+            const float cin = sm.carry[r][n];
             float a[K], bx[K];
 #pragma unroll
             for (int k = 0; k < K; k += 4) {
@@ -156,21 +150,19 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_kernel(FwdParams p) {
                 const float bb[4] = {bv.x, bv.y, bv.z, bv.w};
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
-                    a[k + q] = fast_exp2(fmaf(dt[k + q], A2[n], M[k + q]));
+                    a[k + q] = fast_exp2(fmaf(dt[k + q], A2n, M[k + q]));
                     bx[k + q] = du[k + q] * bb[q];
                 }
             }
             // fold the lane's K tokens into one affine map h -> P h + H
-            float P = a[0], H = bx[0];
+            float H = bx[0];
 #pragma unroll
-            for (int k = 1; k < K; ++k) {
-                H = fmaf(a[k], H, bx[k]);
-                P = P * a[k];
-            }
-            row_scan_fwd(P, H);
-            const float hend = fmaf(P, carry[n], H);          // state after this lane's last token
-            float h = dpp<kRowShr1>(carry[n], hend);          // state before this lane's first token
-            carry[n] = dpp<kNewBcast15>(0.0f, hend);          // state after the chunk
+            for (int k = 1; k < K; ++k) H = fmaf(a[k], H, bx[k]);
+            float P = fast_exp2(fmaf(S, A2n, Mf));
+            row_scan_up(P, H);
+            const float hend = fmaf(P, cin, H);               // state after this lane's last token
+            float h = dpp<kRowShr1>(cin, hend);               // state before this lane's first token
+            if (j == 15) sm.carry[r][n] = hend;               // state after the chunk
 #pragma unroll
             for (int k = 0; k < K; k += 4) {
                 const f32x4 cv = *reinterpret_cast<const f32x4*>(&sm.C[n][j][k]);

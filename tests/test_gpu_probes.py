@@ -72,8 +72,9 @@ def test_scan_probe(key, out_f32):
     assert not dB[:, 1:].any() and not dC[:, 1:].any(), "dB/dC of untouched states"
     dA = host(g["dA"])
     assert not dA[:, 1:].any()
+    # dA sums rem*pos over every token: too large to be exact in fp32, so the fp32 bound applies
     want_dA0 = float(np.sum(np.where(pos != 0, rem * pos, 0.0)))
-    assert np.allclose(dA[:, 0], want_dA0, rtol=1e-6, atol=0), (dA[:4, 0], want_dA0)
+    assert np.all(np.abs(dA[:, 0] - want_dA0) <= 1e-4 * (1 + abs(want_dA0))), (dA[:4, 0], want_dA0)
 
 
 @pytest.mark.parametrize("key,out_f32", [("0", True), ("1", True), ("2", True), ("4a", True),
