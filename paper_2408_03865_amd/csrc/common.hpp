@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 namespace pm {
 
 // ---------------------------------------------------------------------------
@@ -68,12 +70,14 @@ template <> struct Storage<bf16_t> {
 // Load K consecutive elements starting at row[l0] (K a multiple of the vector width),
 // converting to float; elements at or beyond L read as `fill`.  `vec` says the row
 // base is 16-byte aligned and L is a multiple of the vector width.
-template <typename T, int K>
+// With FULL the caller guarantees l0 + K <= L and vector alignment, so the loads are
+// unconditional (no control flow: the compiler can batch them and defer the waits).
+template <typename T, int K, bool FULL = false>
 __device__ __forceinline__ void load_run(const T* __restrict__ row, int64_t l0, int64_t L, bool vec,
                                          float* v, float fill = 0.0f) {
     constexpr int PV = Storage<T>::kPerVec;
     static_assert(K % PV == 0, "K must be a multiple of the vector width");
-    if (vec && l0 + K <= L) {
+    if (FULL || (vec && l0 + K <= L)) {
 #pragma unroll
         for (int i = 0; i < K / PV; ++i) {
             const u32x4 w = *reinterpret_cast<const u32x4*>(row + l0 + i * PV);
@@ -86,11 +90,11 @@ __device__ __forceinline__ void load_run(const T* __restrict__ row, int64_t l0, 
 }
 
 // Store K consecutive elements (rounding to T) at row[l0]; elements beyond L are dropped.
-template <typename T, int K>
+template <typename T, int K, bool FULL = false>
 __device__ __forceinline__ void store_run(T* __restrict__ row, int64_t l0, int64_t L, bool vec,
                                           const float* v) {
     constexpr int PV = Storage<T>::kPerVec;
-    if (vec && l0 + K <= L) {
+    if (FULL || (vec && l0 + K <= L)) {
 #pragma unroll
         for (int i = 0; i < K / PV; ++i)
             *reinterpret_cast<u32x4*>(row + l0 + i * PV) = Storage<T>::pack(v + i * PV);

@@ -30,14 +30,18 @@ constexpr int kCH = 16 * kK;        // tokens per chunk == saved-state stride
 static_assert(kCH == 128, "chunk must equal the saved-state stride");
 static_assert(kRows == kScanBwdChannels, "partials are per 16 channels");
 
+constexpr int kWaves = kThreads / 64;
+constexpr int kSeg = kK + 4;        // padded lane segment: conflict-free 16-byte LDS reads
+
 struct __attribute__((aligned(16))) BwdSmem {
-    float B[kN][16][kK];            // [state][lane][token]
-    float C[kN][16][kK];
-    float M[16][kK];                // 0, or -inf on a sequence start
-    float red[2][2][kRows][kCH];    // [state parity][dB|dC][row][token]
+    float B[kN][16][kSeg];          // [state][lane][token]
+    float C[kN][16][kSeg];
+    float M[16][kSeg];              // 0, or -inf on a sequence start
+    float red[2][kWaves][2][kCH];   // [state parity][wave][dB|dC][token]: per-wave channel sums
     float A2[kRows][kN];            // A * log2(e)
     float xc[kRows][kN];            // dh at the first token of the chunk to the right
     float an[kRows][kN];            // Abar at the first token of the chunk to the right
+    float hin[kRows][kN];           // state at the chunk start (saved by the forward)
     float dA[kRows][kN];            // per-channel dA accumulators
 };
 
@@ -96,7 +100,6 @@ void scan_bwd_kernel(BwdParams p) {
     const T* Bb = static_cast<const T*>(p.B) + b * kN * L;
     const T* Cb = static_cast<const T*>(p.C) + b * kN * L;
     const int32_t* pr = p.pos + b * L;
-    const float* st = p.states + (b * p.dim + d) * (int64_t)p.nchunk_states * kN;
 
     {   // per-channel tables
         const int rr = tid >> 4, n = tid & 15;
@@ -112,14 +115,17 @@ void scan_bwd_kernel(BwdParams p) {
     float dt_next = 0.0f, m_next = 0.0f;     // step and mask of the first token of the chunk to the right
 
     const int64_t nchunk = (L + kCH - 1) / kCH;
-    for (int64_t c = nchunk - 1; c >= 0; --c) {
+    // One chunk; FULL (block-uniform) means the chunk lies inside the row and vector
+    // access is allowed, so every load and store is unconditional.
+    auto chunk = [&](auto full_tag, const int64_t c) {
+        constexpr bool FULL = decltype(full_tag)::value;
         const int64_t lb = c * kCH;
         // ---- stage B, C, the reset mask and the chunk-start states in LDS ----
         for (int idx = tid * PV; idx < kN * kCH; idx += kThreads * PV) {
             const int n = idx / kCH, t = idx - n * kCH;
             float vb[PV], vc[PV];
-            load_run<T, PV>(Bb + (int64_t)n * L, lb + t, L, p.vec, vb);
-            load_run<T, PV>(Cb + (int64_t)n * L, lb + t, L, p.vec, vc);
+            load_run<T, PV, FULL>(Bb + (int64_t)n * L, lb + t, L, p.vec, vb);
+            load_run<T, PV, FULL>(Cb + (int64_t)n * L, lb + t, L, p.vec, vc);
             float* db = &sm.B[n][t / K][t % K];
             float* dc = &sm.C[n][t / K][t % K];
 #pragma unroll
@@ -127,11 +133,14 @@ void scan_bwd_kernel(BwdParams p) {
         }
         for (int t = tid; t < kCH; t += kThreads) {
             const int64_t l = lb + t;
-            sm.M[t / K][t % K] = (l < L && pr[l] == 0) ? -INFINITY : 0.0f;
+            sm.M[t / K][t % K] = ((FULL || l < L) && pr[l] == 0) ? -INFINITY : 0.0f;
+        }
+        {   // state at the chunk start (h after token lb-1), saved by the forward
+            const int rr = tid >> 4, n = tid & 15;
+            const int64_t dd = min((int64_t)g * kRows + rr, p.dim - 1);
+            sm.hin[rr][n] = c > 0 ? p.states[((b * p.dim + dd) * p.nchunk_states + (c - 1)) * kN + n] : 0.0f;
         }
         __syncthreads();
-        // state at the chunk start (h after token lb-1), saved by the forward
-        const float* hin_src = c > 0 ? st + (c - 1) * kN : nullptr;
 
         // ---- per-token inputs ----
         const int64_t l0 = lb + (int64_t)j * K;
@@ -139,12 +148,12 @@ void scan_bwd_kernel(BwdParams p) {
         float S = 0.0f, Mf = 0.0f, Mr = 0.0f, m0 = 0.0f;
         {
             float dl[K], uv[K];
-            load_run<T, K>(ur, l0, L, p.vec, uv);
-            load_run<T, K>(dr, l0, L, p.vec, dl);
-            load_run<T, K>(gr, l0, L, p.vec, dyD);     // dout for now
+            load_run<T, K, FULL>(ur, l0, L, p.vec, uv);
+            load_run<T, K, FULL>(dr, l0, L, p.vec, dl);
+            load_run<T, K, FULL>(gr, l0, L, p.vec, dyD);     // dout for now
             if (zr) {
                 float zv[K];
-                load_run<T, K>(zr, l0, L, p.vec, zv);
+                load_run<T, K, FULL>(zr, l0, L, p.vec, zv);
 #pragma unroll
                 for (int k = 0; k < K; ++k) dyD[k] *= zv[k] * sigmoid_f(zv[k]);   // dy = dout * SiLU(z)
             }
@@ -152,7 +161,7 @@ void scan_bwd_kernel(BwdParams p) {
             for (int k = 0; k < K; ++k) {
                 const float s = dl[k] + dbias;
                 float v = p.softplus ? softplus_f(s) : s;
-                v = (l0 + k < L) ? v : 0.0f;          // identity past the row end
+                if (!FULL) v = (l0 + k < L) ? v : 0.0f;   // identity past the row end
                 dt[k] = v;
                 if (!active) dyD[k] = 0.0f;           // padding rows contribute nothing to dB, dC
                 dlu[k] = active ? v * uv[k] : 0.0f;
@@ -181,13 +190,11 @@ void scan_bwd_kernel(BwdParams p) {
         Mr += m0n;
         dt_next = dpp<kNewBcast0>(0.0f, dt[0]);
         m_next = dpp<kNewBcast0>(0.0f, m0);
-        float hin_next = hin_src ? hin_src[0] : 0.0f;
 
 #pragma unroll 1
         for (int n = 0; n < kN; ++n) {
             const float A2n = sm.A2[r][n];
-            const float hin = hin_next;
-            if (hin_src && n + 1 < kN) hin_next = hin_src[n + 1];     // prefetch one state ahead
+            const float hin = sm.hin[r][n];
             const float xc = sm.xc[r][n];
             const float an = sm.an[r][n];
             float a[K], ah[K], bv[K], cdy[K], bx[K], M[K];
@@ -257,22 +264,38 @@ void scan_bwd_kernel(BwdParams p) {
             dAl = row_sum_to_15(dAl);
             if (j == 15) sm.dA[r][n] += dAl;
             // ---- dB, dC: sum over the block's 16 channels ----
-            float* rb = &sm.red[n & 1][0][r][j * K];
-            float* rc = &sm.red[n & 1][1][r][j * K];
+            // First over the wave's 4 rows (channels) in registers, by a transposed
+            // butterfly: permlane32_swap pairs rows {0,1} with {2,3} and leaves dB sums
+            // on rows 0-1 and dC sums on rows 2-3; permlane16_swap pairs even with odd
+            // rows and leaves token slots 0-3 on even rows and 4-7 on odd rows.
+            float R[K];
 #pragma unroll
-            for (int k = 0; k < K; k += 4) {
-                *reinterpret_cast<f32x4*>(rb + k) = f32x4{dBp[k], dBp[k + 1], dBp[k + 2], dBp[k + 3]};
-                *reinterpret_cast<f32x4*>(rc + k) = f32x4{bx[k], bx[k + 1], bx[k + 2], bx[k + 3]};
+            for (int k = 0; k < K; ++k) {
+                const auto s2 = __builtin_amdgcn_permlane32_swap(__float_as_uint(dBp[k]),
+                                                                 __float_as_uint(bx[k]), false, false);
+                R[k] = __uint_as_float(s2[0]) + __uint_as_float(s2[1]);
+            }
+            float Q[K / 2];
+#pragma unroll
+            for (int k = 0; k < K / 2; ++k) {
+                const auto s2 = __builtin_amdgcn_permlane16_swap(__float_as_uint(R[k]),
+                                                                 __float_as_uint(R[k + K / 2]), false, false);
+                Q[k] = __uint_as_float(s2[0]) + __uint_as_float(s2[1]);
+            }
+            {
+                const int wr = r & 3;                // row inside the wave
+                *reinterpret_cast<f32x4*>(&sm.red[n & 1][tid >> 6][wr >> 1][j * K + (K / 2) * (wr & 1)]) =
+                    f32x4{Q[0], Q[1], Q[2], Q[3]};
             }
             __syncthreads();
-            {
+            {   // then over the block's 4 waves, in a fixed order
                 const int which = tid >> 7;          // 0: dB, 1: dC
                 const int t = tid & (kCH - 1);
                 float s = 0.0f;
 #pragma unroll
-                for (int q = 0; q < kRows; ++q) s += sm.red[n & 1][which][q][t];
+                for (int q = 0; q < kWaves; ++q) s += sm.red[n & 1][q][which][t];
                 const int64_t l = lb + t;
-                if (l < L)
+                if (FULL || l < L)
                     p.part_bc[(((b * p.groups + g) * 2 + which) * kN + n) * L + l] = s;
             }
             // no second barrier: the next state writes the other buffer, and this one is
@@ -283,8 +306,8 @@ void scan_bwd_kernel(BwdParams p) {
         float o_du[K], o_dd[K];
         {
             float dl[K], uv[K];
-            load_run<T, K>(dr, l0, L, p.vec, dl);
-            load_run<T, K>(ur, l0, L, p.vec, uv);
+            load_run<T, K, FULL>(dr, l0, L, p.vec, dl);
+            load_run<T, K, FULL>(ur, l0, L, p.vec, uv);
 #pragma unroll
             for (int k = 0; k < K; ++k) {
                 o_du[k] = fmaf(dyD[k], Dd, dt[k] * sdhB[k]);
@@ -293,25 +316,29 @@ void scan_bwd_kernel(BwdParams p) {
                 const float gs = p.softplus ? (s > 20.0f ? 1.0f : sigmoid_f(s)) : 1.0f;
                 o_dd[k] = ddt * gs;
                 dDacc = fmaf(dyD[k], uv[k], dDacc);
-                dbacc += (l0 + k < L) ? o_dd[k] : 0.0f;
+                dbacc += (FULL || l0 + k < L) ? o_dd[k] : 0.0f;
             }
         }
         if (active) {
-            store_run<TO, K>(dur, l0, L, p.vec, o_du);
-            store_run<TO, K>(ddr, l0, L, p.vec, o_dd);
+            store_run<TO, K, FULL>(dur, l0, L, p.vec, o_du);
+            store_run<TO, K, FULL>(ddr, l0, L, p.vec, o_dd);
             if (dzr) {
                 float zv[K], gv[K], o_dz[K];
-                load_run<T, K>(zr, l0, L, p.vec, zv);
-                load_run<T, K>(gr, l0, L, p.vec, gv);
+                load_run<T, K, FULL>(zr, l0, L, p.vec, zv);
+                load_run<T, K, FULL>(gr, l0, L, p.vec, gv);
 #pragma unroll
                 for (int k = 0; k < K; ++k) {
                     const float sz = sigmoid_f(zv[k]);
                     o_dz[k] = gv[k] * yacc[k] * sz * (1.0f + zv[k] * (1.0f - sz));
                 }
-                store_run<TO, K>(dzr, l0, L, p.vec, o_dz);
+                store_run<TO, K, FULL>(dzr, l0, L, p.vec, o_dz);
             }
         }
         __syncthreads();     // LDS is restaged for the next chunk
+    };
+    for (int64_t c = nchunk - 1; c >= 0; --c) {
+        if (p.vec && (c + 1) * kCH <= L) chunk(std::true_type{}, c);
+        else chunk(std::false_type{}, c);
     }
 
     // ---- per-channel partials ----

@@ -32,9 +32,12 @@ constexpr int kStride = 128;        // saved-state token stride (PACKMAMBA_STATE
 
 template <int K>
 struct __attribute__((aligned(16))) FwdSmem {
-    float B[kN][16][K];         // [state][lane][token]
-    float C[kN][16][K];
-    float M[16][K];             // 0, or -inf on a sequence start
+    // [state][lane][token], each lane's segment padded by 4 floats so that the
+    // 16-byte reads of 8 consecutive lanes fall in distinct banks
+    static constexpr int kSeg = K + 4;
+    float B[kN][16][kSeg];
+    float C[kN][16][kSeg];
+    float M[16][kSeg];          // 0, or -inf on a sequence start
     float A2[kRows][kN];        // A * log2(e)
     float carry[kRows][kN];     // state after the previous chunk
 };
@@ -92,14 +95,17 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_kernel(FwdParams p) {
     const float dbias = p.delta_bias ? p.delta_bias[d] : 0.0f;
 
     const int64_t nchunk = (L + CH - 1) / CH;
-    for (int64_t c = 0; c < nchunk; ++c) {
+    // One chunk; FULL (block-uniform) means the chunk lies inside the row and vector
+    // access is allowed, so every load and store is unconditional.
+    auto chunk = [&](auto full_tag, const int64_t c) {
+        constexpr bool FULL = decltype(full_tag)::value;
         const int64_t lb = c * CH;
         // ---- stage B, C and the reset mask of this chunk in LDS ----
         for (int idx = tid * PV; idx < kN * CH; idx += kThreads * PV) {
             const int n = idx / CH, t = idx - n * CH;
             float vb[PV], vc[PV];
-            load_run<T, PV>(Bb + (int64_t)n * L, lb + t, L, p.vec, vb);
-            load_run<T, PV>(Cb + (int64_t)n * L, lb + t, L, p.vec, vc);
+            load_run<T, PV, FULL>(Bb + (int64_t)n * L, lb + t, L, p.vec, vb);
+            load_run<T, PV, FULL>(Cb + (int64_t)n * L, lb + t, L, p.vec, vc);
             float* db = &sm.B[n][t / K][t % K];
             float* dc = &sm.C[n][t / K][t % K];
 #pragma unroll
@@ -107,7 +113,7 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_kernel(FwdParams p) {
         }
         for (int t = tid; t < CH; t += kThreads) {
             const int64_t l = lb + t;
-            sm.M[t / K][t % K] = (l < L && pr[l] == 0) ? -INFINITY : 0.0f;
+            sm.M[t / K][t % K] = ((FULL || l < L) && pr[l] == 0) ? -INFINITY : 0.0f;
         }
         __syncthreads();
 
@@ -116,13 +122,13 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_kernel(FwdParams p) {
         float dt[K], du[K], y[K], M[K];
         {
             float uv[K];
-            load_run<T, K>(ur, l0, L, p.vec, uv);
-            load_run<T, K>(dr, l0, L, p.vec, dt);
+            load_run<T, K, FULL>(ur, l0, L, p.vec, uv);
+            load_run<T, K, FULL>(dr, l0, L, p.vec, dt);
 #pragma unroll
             for (int k = 0; k < K; ++k) {
                 const float s = dt[k] + dbias;
                 float v = p.softplus ? softplus_f(s) : s;
-                v = (l0 + k < L) ? v : 0.0f;       // identity past the row end
+                if (!FULL) v = (l0 + k < L) ? v : 0.0f;   // identity past the row end
                 dt[k] = v;
                 du[k] = v * uv[k];
                 y[k] = Dd * uv[k];
@@ -185,13 +191,17 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_kernel(FwdParams p) {
         if (orow && active) {
             if (zr) {
                 float zv[K];
-                load_run<T, K>(zr, l0, L, p.vec, zv);
+                load_run<T, K, FULL>(zr, l0, L, p.vec, zv);
 #pragma unroll
                 for (int k = 0; k < K; ++k) y[k] = y[k] * zv[k] * sigmoid_f(zv[k]);
             }
-            store_run<TO, K>(orow, l0, L, p.vec, y);
+            store_run<TO, K, FULL>(orow, l0, L, p.vec, y);
         }
         __syncthreads();      // LDS is restaged for the next chunk
+    };
+    for (int64_t c = 0; c < nchunk; ++c) {
+        if (p.vec && (c + 1) * CH <= L) chunk(std::true_type{}, c);
+        else chunk(std::false_type{}, c);
     }
 }
 
