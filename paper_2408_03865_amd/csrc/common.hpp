@@ -129,23 +129,24 @@ __device__ __forceinline__ float dpp(float old, float v) {
 // move into a VOP2 consumer when the move's `old` operand is a constant, so these
 // are written directly; a lane whose source is outside its row is disabled and
 // keeps its value, which is the identity of each operation.  gfx9 needs two wait
-// states between a VALU write of a VGPR and a DPP read of it; the `s_nop 1` on
-// both sides covers writes by surrounding compiler-generated code as well.
+// states between a VALU write of a VGPR and a DPP read of it: each op starts with
+// `s_nop 1`, and each sequence below ends with one, so DPP reads issued by the
+// surrounding compiler-generated code are covered too.
 #define PM_DPP_OPS(NAME, CTRL)                                                              \
     __device__ __forceinline__ void mul_##NAME(float& x) { /* x = x[src] * x */            \
         asm("s_nop 1\n\tv_mul_f32_dpp %0, %0, %0 " CTRL                           \
-                     " row_mask:0xf bank_mask:0xf\n\ts_nop 1"                                \
+                     " row_mask:0xf bank_mask:0xf"                                \
                      : "+v"(x));                                                            \
     }                                                                                       \
     __device__ __forceinline__ void fmac_##NAME(float& h, float p) { /* h = h[src] * p + h */ \
         asm("s_nop 1\n\tv_fmac_f32_dpp %0, %0, %1 " CTRL                          \
-                     " row_mask:0xf bank_mask:0xf\n\ts_nop 1"                                \
+                     " row_mask:0xf bank_mask:0xf"                                \
                      : "+v"(h)                                                              \
                      : "v"(p));                                                             \
     }                                                                                       \
     __device__ __forceinline__ void add_##NAME(float& x) { /* x = x[src] + x */            \
         asm("s_nop 1\n\tv_add_f32_dpp %0, %0, %0 " CTRL                           \
-                     " row_mask:0xf bank_mask:0xf\n\ts_nop 1"                                \
+                     " row_mask:0xf bank_mask:0xf"                                \
                      : "+v"(x));                                                            \
     }
 PM_DPP_OPS(shr1, "row_shr:1")
@@ -162,21 +163,26 @@ PM_DPP_OPS(shl8, "row_shl:8")
 // Forward (towards higher lanes): lane j ends with the composition of lanes 0..j
 // (lane j's map applied last).  Reverse: lane j ends with the composition of
 // lanes 15..j (lane j's map applied last).
+__device__ __forceinline__ void dpp_tail_nop(float& x) { asm("s_nop 1" : "+v"(x)); }
+
 __device__ __forceinline__ void row_scan_up(float& P, float& H) {
     fmac_shr1(H, P); mul_shr1(P);
     fmac_shr2(H, P); mul_shr2(P);
     fmac_shr4(H, P); mul_shr4(P);
     fmac_shr8(H, P); mul_shr8(P);
+    dpp_tail_nop(P);
 }
 __device__ __forceinline__ void row_scan_down(float& P, float& H) {
     fmac_shl1(H, P); mul_shl1(P);
     fmac_shl2(H, P); mul_shl2(P);
     fmac_shl4(H, P); mul_shl4(P);
     fmac_shl8(H, P); mul_shl8(P);
+    dpp_tail_nop(P);
 }
 // Sum over the 16 lanes of a row, delivered to lane 15.
 __device__ __forceinline__ float row_sum_to_15(float x) {
     add_shr1(x); add_shr2(x); add_shr4(x); add_shr8(x);
+    dpp_tail_nop(x);
     return x;
 }
 

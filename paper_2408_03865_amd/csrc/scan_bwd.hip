@@ -356,21 +356,33 @@ void scan_bwd_kernel(BwdParams p) {
     }
 }
 
-// dB[b,n,l] / dC[b,n,l] = sum over groups of the per-block partials (fixed order)
+// dB[b,n,l] / dC[b,n,l] = sum over groups of the per-block partials.  Each thread owns
+// four consecutive tokens and keeps four running sums over interleaved groups
+// (q mod 4), added at the end: a fixed order, so the result is reproducible.
 __global__ void scan_bwd_finalize_bc(const float* __restrict__ part, float* __restrict__ dB,
                                      float* __restrict__ dC, int64_t batch, int64_t L,
                                      int groups) {
     const int64_t NL = (int64_t)kN * L;
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;   // over batch*2*NL
-    if (i >= batch * 2 * NL) return;
-    const int64_t b = i / (2 * NL);
-    const int64_t rem = i - b * 2 * NL;
+    const int64_t i4 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;   // over batch*2*NL
+    if (i4 >= batch * 2 * NL) return;
+    const int64_t b = i4 / (2 * NL);
+    const int64_t rem = i4 - b * 2 * NL;
     const int which = (int)(rem / NL);
     const int64_t nl = rem - which * NL;
     const float* src = part + ((b * groups) * 2 + which) * NL + nl;
-    float s = 0.0f;
-    for (int q = 0; q < groups; ++q) s += src[(int64_t)q * 2 * NL];
-    (which ? dC : dB)[b * NL + nl] = s;
+    const int64_t stride = 2 * NL;
+    float* dst = (which ? dC : dB) + b * NL + nl;
+    // NL = 16 L, so a group of four never crosses a (b, dB|dC) boundary and every
+    // offset is a multiple of four floats (16-byte aligned).
+    f32x4 acc[4] = {};
+    int q = 0;
+    for (; q + 4 <= groups; q += 4) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            acc[u] += *reinterpret_cast<const f32x4*>(src + (int64_t)(q + u) * stride);
+    }
+    for (; q < groups; ++q) acc[q & 3] += *reinterpret_cast<const f32x4*>(src + (int64_t)q * stride);
+    *reinterpret_cast<f32x4*>(dst) = (acc[0] + acc[1]) + (acc[2] + acc[3]);
 }
 
 // dA[d,n], dD[d], ddelta_bias[d] = sum over batch rows (fixed order)
@@ -403,8 +415,8 @@ hipError_t launch_t(const ScanArgs& a, hipStream_t s) {
     hipLaunchKernelGGL((scan_bwd_kernel<T, TO>), grid, dim3(kThreads), 0, s, p);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const int64_t nbc = a.batch * 2 * kN * a.seqlen;
-    hipLaunchKernelGGL(scan_bwd_finalize_bc, dim3((unsigned)((nbc + 255) / 256)), dim3(256), 0, s,
+    const int64_t nbc4 = (a.batch * 2 * kN * a.seqlen + 3) / 4;
+    hipLaunchKernelGGL(scan_bwd_finalize_bc, dim3((unsigned)((nbc4 + 255) / 256)), dim3(256), 0, s,
                        a.part_bc, a.dB, a.dC, a.batch, a.seqlen, p.groups);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
