@@ -42,6 +42,7 @@ struct __attribute__((aligned(16))) BwdSmem {
     float xc[kRows][kN];            // dh at the first token of the chunk to the right
     float an[kRows][kN];            // Abar at the first token of the chunk to the right
     float hin[kRows][kN];           // state at the chunk start (saved by the forward)
+    float gz[kThreads][kK];         // per token: dout * d(z sigmoid(z))/dz, for dz at the chunk end
     float dA[kRows][kN];            // per-channel dA accumulators
 };
 
@@ -152,20 +153,28 @@ void scan_bwd_kernel(BwdParams p) {
             load_run<T, K, FULL>(dr, l0, L, p.vec, dl);
             load_run<T, K, FULL>(gr, l0, L, p.vec, dyD);     // dout for now
             if (zr) {
-                float zv[K];
+                float zv[K], gz[K];
                 load_run<T, K, FULL>(zr, l0, L, p.vec, zv);
 #pragma unroll
-                for (int k = 0; k < K; ++k) dyD[k] *= zv[k] * sigmoid_f(zv[k]);   // dy = dout * SiLU(z)
+                for (int k = 0; k < K; ++k) {
+                    const float sz = sigmoid_f(zv[k]);
+                    gz[k] = dyD[k] * sz * (1.0f + zv[k] * (1.0f - sz));    // dz = gz * (y + D u)
+                    dyD[k] *= zv[k] * sz;                                 // dy = dout * SiLU(z)
+                }
+                *reinterpret_cast<f32x4*>(&sm.gz[tid][0]) = f32x4{gz[0], gz[1], gz[2], gz[3]};
+                *reinterpret_cast<f32x4*>(&sm.gz[tid][4]) = f32x4{gz[4], gz[5], gz[6], gz[7]};
             }
 #pragma unroll
             for (int k = 0; k < K; ++k) {
                 const float s = dl[k] + dbias;
-                float v = p.softplus ? softplus_f(s) : s;
+                float v = s;
+                if (p.softplus) v = softplus_f(s);
                 if (!FULL) v = (l0 + k < L) ? v : 0.0f;   // identity past the row end
                 dt[k] = v;
                 if (!active) dyD[k] = 0.0f;           // padding rows contribute nothing to dB, dC
                 dlu[k] = active ? v * uv[k] : 0.0f;
                 yacc[k] = Dd * uv[k];
+                dDacc = fmaf(dyD[k], uv[k], dDacc);
                 sdhB[k] = 0.0f;
                 sdA[k] = 0.0f;
             }
@@ -305,17 +314,15 @@ void scan_bwd_kernel(BwdParams p) {
         // ---- per-token gradients ----
         float o_du[K], o_dd[K];
         {
-            float dl[K], uv[K];
-            load_run<T, K, FULL>(dr, l0, L, p.vec, dl);
+            float uv[K], dl[K];
             load_run<T, K, FULL>(ur, l0, L, p.vec, uv);
+            load_run<T, K, FULL>(dr, l0, L, p.vec, dl);
 #pragma unroll
             for (int k = 0; k < K; ++k) {
                 o_du[k] = fmaf(dyD[k], Dd, dt[k] * sdhB[k]);
                 const float ddt = fmaf(uv[k], sdhB[k], sdA[k] * kLn2);   // sdA was built with A*log2e
                 const float s = dl[k] + dbias;
-                const float gs = p.softplus ? (s > 20.0f ? 1.0f : sigmoid_f(s)) : 1.0f;
-                o_dd[k] = ddt * gs;
-                dDacc = fmaf(dyD[k], uv[k], dDacc);
+                o_dd[k] = ddt * (p.softplus ? (s > 20.0f ? 1.0f : sigmoid_f(s)) : 1.0f);
                 dbacc += (FULL || l0 + k < L) ? o_dd[k] : 0.0f;
             }
         }
@@ -323,14 +330,12 @@ void scan_bwd_kernel(BwdParams p) {
             store_run<TO, K, FULL>(dur, l0, L, p.vec, o_du);
             store_run<TO, K, FULL>(ddr, l0, L, p.vec, o_dd);
             if (dzr) {
-                float zv[K], gv[K], o_dz[K];
-                load_run<T, K, FULL>(zr, l0, L, p.vec, zv);
-                load_run<T, K, FULL>(gr, l0, L, p.vec, gv);
+                float o_dz[K];
+                const f32x4 g0 = *reinterpret_cast<const f32x4*>(&sm.gz[tid][0]);
+                const f32x4 g1 = *reinterpret_cast<const f32x4*>(&sm.gz[tid][4]);
+                const float gz[K] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
 #pragma unroll
-                for (int k = 0; k < K; ++k) {
-                    const float sz = sigmoid_f(zv[k]);
-                    o_dz[k] = gv[k] * yacc[k] * sz * (1.0f + zv[k] * (1.0f - sz));
-                }
+                for (int k = 0; k < K; ++k) o_dz[k] = gz[k] * yacc[k];
                 store_run<TO, K, FULL>(dzr, l0, L, p.vec, o_dz);
             }
         }
