@@ -149,6 +149,7 @@ def main():
     nst = (L + _lib.STATE_STRIDE - 1) // _lib.STATE_STRIDE
     states = torch.empty((Nb, Dn, nst, N), dtype=torch.float32, device=dev)
     ws_scan = torch.empty(lib.packmamba_selective_scan_bwd_workspace_size(Nb, Dn, L, N), dtype=torch.uint8, device=dev)
+    ws_fwd = torch.empty(max(1, lib.packmamba_selective_scan_fwd_workspace_size(Nb, Dn, L, N)), dtype=torch.uint8, device=dev)
     ws_conv = torch.empty(lib.packmamba_causal_conv1d_bwd_workspace_size(Nb, Dn, L, Wd), dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream(dev)
     sp = stream.cuda_stream
@@ -159,7 +160,8 @@ def main():
 
     def scan_fwd():
         _lib.check("scan_fwd", lib.packmamba_selective_scan_fwd(
-            P(u), P(dl), P(A), P(B), P(C), P(D), P(z), P(dbias), 1, P(pos), P(out), P(states), Nb, Dn, L, N, code, sp))
+            P(u), P(dl), P(A), P(B), P(C), P(D), P(z), P(dbias), 1, P(pos), P(out), P(states),
+            P(ws_fwd), ws_fwd.numel(), Nb, Dn, L, N, code, sp))
 
     def scan_bwd():
         _lib.check("scan_bwd", lib.packmamba_selective_scan_bwd(

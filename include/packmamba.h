@@ -45,7 +45,7 @@
 extern "C" {
 #endif
 
-#define PACKMAMBA_ABI_VERSION 1
+#define PACKMAMBA_ABI_VERSION 2
 
 /* dtype codes of the activation tensors */
 #define PACKMAMBA_F32 0            /* fp32 inputs, fp32 outputs */
@@ -111,6 +111,13 @@ int packmamba_causal_conv1d_bwd(const void* x, const float* weight, const float*
 size_t packmamba_selective_scan_fwd_saved_states_size(int64_t batch, int64_t dim, int64_t seqlen,
                                                       int32_t dstate);
 
+/* Bytes of workspace packmamba_selective_scan_fwd needs: nonzero only for shapes
+ * whose rows are split into segments scanned by separate blocks (long rows with
+ * few batch rows and channels: fewer than 768 blocks of 16 channels); 0 when none
+ * is needed or the shape is invalid (the call itself reports the latter). */
+size_t packmamba_selective_scan_fwd_workspace_size(int64_t batch, int64_t dim, int64_t seqlen,
+                                                   int32_t dstate);
+
 /*
  * Packed selective scan, forward (Eqs. 1a, 1b, 2a; Alg. 2; §3.4).
  *   dt[b,d,l]   = softplus(delta[b,d,l] + delta_bias[d])   (softplus if delta_softplus,
@@ -126,11 +133,15 @@ size_t packmamba_selective_scan_fwd_saved_states_size(int64_t batch, int64_t dim
  *   token min((c+1)*PACKMAMBA_STATE_STRIDE, seqlen)-1 for every chunk c, laid out
  *   (batch, dim, chunk, dstate); the backward reuses it instead of recomputing.
  *   `out` may be NULL when saved_states is not (states only).
+ *   workspace: device scratch of packmamba_selective_scan_fwd_workspace_size()
+ *   bytes, owned by the caller and not read after the call's kernels finish; may
+ *   be NULL when that size is 0.  Too small or missing: PACKMAMBA_ERR_WORKSPACE.
  */
 int packmamba_selective_scan_fwd(const void* u, const void* delta, const float* A,
                                  const void* B, const void* C, const float* D, const void* z,
                                  const float* delta_bias, int32_t delta_softplus,
                                  const int32_t* position_indices, void* out, float* saved_states,
+                                 void* workspace, size_t workspace_bytes,
                                  int64_t batch, int64_t dim, int64_t seqlen, int32_t dstate,
                                  int32_t dtype, void* stream);
 

@@ -21,7 +21,7 @@ from ._lib import BF16, BF16_F32OUT, F32, STATE_STRIDE, PackMambaError, load
 
 __all__ = [
     "causal_conv1d_fwd", "causal_conv1d_bwd", "selective_scan_fwd", "selective_scan_bwd",
-    "check_position_indices", "saved_states_size", "PackMambaError", "load", "F32", "BF16",
+    "check_position_indices", "saved_states_size", "segments", "PackMambaError", "load", "F32", "BF16",
     "STATE_STRIDE", "BF16_F32OUT",
 ]
 
@@ -87,23 +87,39 @@ def causal_conv1d_bwd(x, weight, bias, position_indices, dout, silu: bool = True
     return dx, dw, db
 
 
+def segments(batch: int, dim: int, seqlen: int) -> int:
+    """Segments per row the scans use for this shape (1: rows are not split).  Mirrors
+    the rule of the library's launchers, for tests and reports only."""
+    blocks = batch * ((dim + 15) // 16)
+    units = (seqlen + 255) // 256
+    if blocks * 2 >= 1536 or units < 2:
+        return 1
+    nseg = min((1536 + blocks - 1) // blocks, units)
+    per = (units + nseg - 1) // nseg
+    return (units + per - 1) // per
+
+
 def saved_states_size(batch: int, dim: int, seqlen: int, dstate: int = 16) -> int:
     return int(load().packmamba_selective_scan_fwd_saved_states_size(batch, dim, seqlen, dstate))
 
 
 def selective_scan_fwd(u, delta, A, B, C, D, z, delta_bias, delta_softplus, position_indices,
-                       return_states: bool = False, out=True, out_f32: bool = False):
+                       return_states: bool = False, out=True, out_f32: bool = False, workspace=None):
     torch = _torch()
     Nb, Dn, L = u.shape
     N = A.shape[1]
+    lib = load()
     o = _empty_out(u, out_f32) if out else None
+    need = int(lib.packmamba_selective_scan_fwd_workspace_size(Nb, Dn, L, N))
+    ws = workspace if workspace is not None or need == 0 else _workspace(need, u.device)
     states = None
     if return_states:
         nch = (L + STATE_STRIDE - 1) // STATE_STRIDE
         states = torch.empty((Nb, Dn, nch, N), dtype=torch.float32, device=u.device)
-    st = load().packmamba_selective_scan_fwd(
+    st = lib.packmamba_selective_scan_fwd(
         _p(u), _p(delta), _p(A), _p(B), _p(C), _p(D), _p(z), _p(delta_bias), int(delta_softplus),
-        _p(position_indices), _p(o), _p(states), Nb, Dn, L, N, _code(u, out_f32), _stream(u))
+        _p(position_indices), _p(o), _p(states), _p(ws), 0 if ws is None else ws.numel(),
+        Nb, Dn, L, N, _code(u, out_f32), _stream(u))
     _lib.check("packmamba_selective_scan_fwd", st)
     return (o, states) if return_states else o
 

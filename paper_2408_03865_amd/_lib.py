@@ -15,7 +15,7 @@ LIB_PATH = os.path.join(HERE, "libpackmamba.so")
 
 F32, BF16, BF16_F32OUT = 0, 1, 2
 STATE_STRIDE = 128
-ABI_VERSION = 1
+ABI_VERSION = 2
 
 STATUS = {0: "OK", 1: "ERR_NULL", 2: "ERR_SHAPE", 3: "ERR_UNSUPPORTED", 4: "ERR_ALIGN",
           5: "ERR_WORKSPACE", 6: "ERR_LAUNCH"}
@@ -25,8 +25,9 @@ EXPORTS = (
     "packmamba_abi_version", "packmamba_status_string",
     "packmamba_causal_conv1d_fwd", "packmamba_causal_conv1d_bwd_workspace_size",
     "packmamba_causal_conv1d_bwd", "packmamba_selective_scan_fwd_saved_states_size",
-    "packmamba_selective_scan_fwd", "packmamba_selective_scan_bwd_workspace_size",
-    "packmamba_selective_scan_bwd", "packmamba_check_position_indices",
+    "packmamba_selective_scan_fwd_workspace_size", "packmamba_selective_scan_fwd",
+    "packmamba_selective_scan_bwd_workspace_size", "packmamba_selective_scan_bwd",
+    "packmamba_check_position_indices",
 )
 
 
@@ -57,7 +58,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.packmamba_causal_conv1d_bwd.argtypes = [vp] * 9 + [sz, i64, i64, i64, i32, i32, i32, vp]
     lib.packmamba_selective_scan_fwd_saved_states_size.argtypes = [i64, i64, i64, i32]
     lib.packmamba_selective_scan_fwd_saved_states_size.restype = sz
-    lib.packmamba_selective_scan_fwd.argtypes = [vp] * 8 + [i32, vp, vp, vp, i64, i64, i64, i32, i32, vp]
+    lib.packmamba_selective_scan_fwd_workspace_size.argtypes = [i64, i64, i64, i32]
+    lib.packmamba_selective_scan_fwd_workspace_size.restype = sz
+    lib.packmamba_selective_scan_fwd.argtypes = [vp] * 8 + [i32, vp, vp, vp, vp, sz, i64, i64, i64, i32, i32, vp]
     lib.packmamba_selective_scan_bwd_workspace_size.argtypes = [i64, i64, i64, i32]
     lib.packmamba_selective_scan_bwd_workspace_size.restype = sz
     lib.packmamba_selective_scan_bwd.argtypes = ([vp] * 8 + [i32] + [vp] * 12 + [sz, i64, i64, i64, i32, i32, vp])

@@ -36,17 +36,45 @@ int64_t state_chunks(int64_t seqlen) {
     return (seqlen + PACKMAMBA_STATE_STRIDE - 1) / PACKMAMBA_STATE_STRIDE;
 }
 
+// Segment split workspace, shared by both directions: the per-segment maps
+// (batch, dim, nseg, kN, 2) followed by the chained carries (batch, dim, nseg, kN).
+// Empty when the rows are not split.
+struct SegWs {
+    size_t agg, carry, total;
+};
+
+SegWs seg_ws(int64_t batch, int64_t dim, int64_t seqlen) {
+    const pm::SegPlan sp = pm::scan_segments(batch, dim, seqlen);
+    SegWs w{0, 0, 0};
+    if (sp.nseg > 1) {
+        w.agg = align_up(sizeof(float) * (size_t)(batch * dim * sp.nseg * kN * 2));
+        w.carry = align_up(sizeof(float) * (size_t)(batch * dim * sp.nseg * kN));
+        w.total = w.agg + w.carry;
+    }
+    return w;
+}
+
+void set_seg_ws(pm::ScanArgs& a, char* base, const SegWs& w) {
+    a.ws_agg = w.total ? reinterpret_cast<float*>(base) : nullptr;
+    a.ws_carry = w.total ? reinterpret_cast<float*>(base + w.agg) : nullptr;
+}
+
+// Backward workspace: dB/dC partials, per-channel partials, recomputed chunk
+// states (used when no saved states are passed), then the segment workspace.
 struct ScanWs {
     size_t part_bc, part_chan, states, total;
+    SegWs seg;
 };
 
 ScanWs scan_ws(int64_t batch, int64_t dim, int64_t seqlen) {
     const int64_t groups = (dim + pm::kScanBwdChannels - 1) / pm::kScanBwdChannels;
+    const int64_t nseg = pm::scan_segments(batch, dim, seqlen).nseg;
     ScanWs w;
     w.part_bc = align_up(sizeof(float) * (size_t)(batch * groups * 2 * kN * seqlen));
-    w.part_chan = align_up(sizeof(float) * (size_t)(batch * dim * (kN + 2)));
+    w.part_chan = align_up(sizeof(float) * (size_t)(batch * nseg * dim * (kN + 2)));
     w.states = align_up(sizeof(float) * (size_t)(batch * dim * state_chunks(seqlen) * kN));
-    w.total = w.part_bc + w.part_chan + w.states;
+    w.seg = seg_ws(batch, dim, seqlen);
+    w.total = w.part_bc + w.part_chan + w.states + w.seg.total;
     return w;
 }
 
@@ -125,12 +153,19 @@ size_t packmamba_selective_scan_fwd_saved_states_size(int64_t batch, int64_t dim
     return sizeof(float) * (size_t)(batch * dim * state_chunks(seqlen) * kN);
 }
 
+size_t packmamba_selective_scan_fwd_workspace_size(int64_t batch, int64_t dim, int64_t seqlen,
+                                                   int32_t dstate) {
+    if (check_shape(batch, dim, seqlen) || dstate != kN) return 0;
+    return seg_ws(batch, dim, seqlen).total;
+}
+
 int packmamba_selective_scan_fwd(const void* u, const void* delta, const float* A, const void* B,
                                  const void* C, const float* D, const void* z,
                                  const float* delta_bias, int32_t delta_softplus,
                                  const int32_t* position_indices, void* out, float* saved_states,
-                                 int64_t batch, int64_t dim, int64_t seqlen, int32_t dstate,
-                                 int32_t dtype, void* stream) {
+                                 void* workspace, size_t workspace_bytes, int64_t batch,
+                                 int64_t dim, int64_t seqlen, int32_t dstate, int32_t dtype,
+                                 void* stream) {
     if (!u || !delta || !A || !B || !C || !position_indices) return PACKMAMBA_ERR_NULL;
     if (!out && !saved_states) return PACKMAMBA_ERR_NULL;
     if (int e = check_shape(batch, dim, seqlen)) return e;
@@ -138,9 +173,13 @@ int packmamba_selective_scan_fwd(const void* u, const void* delta, const float* 
     if (dstate != kN) return PACKMAMBA_ERR_UNSUPPORTED;
     if (!aligned16(u) || !aligned16(delta) || !aligned16(A) || !aligned16(B) || !aligned16(C) ||
         !aligned16(D) || !aligned16(z) || !aligned16(delta_bias) ||
-        !aligned16(position_indices) || !aligned16(out) || !aligned16(saved_states))
+        !aligned16(position_indices) || !aligned16(out) || !aligned16(saved_states) ||
+        !aligned16(workspace))
         return PACKMAMBA_ERR_ALIGN;
+    const SegWs w = seg_ws(batch, dim, seqlen);
+    if (w.total && (!workspace || workspace_bytes < w.total)) return PACKMAMBA_ERR_WORKSPACE;
     pm::ScanArgs a{};
+    set_seg_ws(a, static_cast<char*>(workspace), w);
     a.u = u; a.delta = delta; a.A = A; a.B = B; a.C = C; a.D = D; a.z = z;
     a.delta_bias = delta_bias; a.pos = position_indices; a.softplus = delta_softplus ? 1 : 0;
     a.out = out; a.states = saved_states;
@@ -183,6 +222,9 @@ int packmamba_selective_scan_bwd(const void* u, const void* delta, const float* 
     a.delta_bias = delta_bias; a.pos = position_indices; a.softplus = delta_softplus ? 1 : 0;
     a.batch = batch; a.dim = dim; a.seqlen = seqlen; a.dstate = dstate; a.dtype = dtype;
     hipStream_t s = (hipStream_t)stream;
+    // the forward recompute below and the backward run one after the other on the
+    // stream, so they share the segment workspace
+    set_seg_ws(a, ws + w.part_bc + w.part_chan + w.states, w.seg);
     if (saved_states) {
         a.states = const_cast<float*>(saved_states);
     } else {

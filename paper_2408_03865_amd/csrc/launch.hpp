@@ -50,13 +50,37 @@ struct ScanArgs {
     float* dD;
     float* ddelta_bias;
     float* part_bc;         // (batch, groups, 2, dstate, seqlen)
-    float* part_chan;       // (batch, dim, dstate + 2)
+    float* part_chan;       // (batch, nseg, dim, dstate + 2)
+    // segment split (both directions): per-segment maps and the chained carries
+    float* ws_agg;          // (batch, dim, nseg, dstate, 2)
+    float* ws_carry;        // (batch, dim, nseg, dstate)
     int64_t batch, dim, seqlen;
     int32_t dstate, dtype;
 };
 
 // channels reduced on chip per dB/dC partial in the backward
 constexpr int kScanBwdChannels = 16;
+
+// Split of the rows into segments along the sequence, each scanned by its own
+// block with the carry across segments resolved by an aggregate pass and a carry
+// pass.  Used only when batch x (channel groups of 16) leaves the GPU underfilled:
+// 256 CUs hold three scan blocks each, and two blocks per slot are wanted.
+struct SegPlan {
+    int64_t nseg;      // segments per row (1: no split)
+    int64_t seg_len;   // tokens per segment, a multiple of kSegUnit
+};
+constexpr int64_t kSegUnit = 256;          // forward chunk, a multiple of the backward chunk
+constexpr int64_t kSegTargetBlocks = 1536;
+
+inline SegPlan scan_segments(int64_t batch, int64_t dim, int64_t seqlen) {
+    const int64_t blocks = batch * ((dim + 15) / 16);
+    const int64_t units = (seqlen + kSegUnit - 1) / kSegUnit;
+    if (blocks * 2 >= kSegTargetBlocks || units < 2) return {1, units * kSegUnit};
+    int64_t nseg = (kSegTargetBlocks + blocks - 1) / blocks;
+    if (nseg > units) nseg = units;
+    const int64_t per = (units + nseg - 1) / nseg;
+    return {(units + per - 1) / per, per * kSegUnit};
+}
 
 hipError_t launch_scan_fwd(const ScanArgs& a, hipStream_t s);
 hipError_t launch_scan_bwd(const ScanArgs& a, hipStream_t s);

@@ -16,6 +16,11 @@
 //     contributions; these are summed over the block's 16 channels in LDS and
 //     written as one partial per block (part_bc), summed over blocks by
 //     scan_bwd_finalize_bc in a fixed order.
+// Long rows with few channels are split into segments scanned by different blocks
+// (as in the forward): an aggregate pass folds each segment's reverse recurrence
+// into dh_first = Q x + H, where x is dh at the first token of the next segment,
+// a carry pass chains them from the row end, and the main pass enters each
+// segment with its chained x.
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -62,13 +67,32 @@ struct BwdParams {
     void* ddelta;
     void* dz;
     float* part_bc;       // (batch, groups, 2, kN, L)
-    float* part_chan;     // (batch, dim, kN + 2): dA[n], dD, ddelta_bias
+    float* part_chan;     // (batch, nseg, dim, kN + 2): dA[n], dD, ddelta_bias
+    float* agg;           // aggregate pass output: (batch, dim, nseg, kN, 2) = (Q, H)
+    const float* xc_in;   // main pass: dh at the first token of the next segment, or null
     int64_t dim, L;
+    int64_t seg_chunks;   // chunks per segment
+    int nseg;
     int nchunk_states;
     int groups;
     int softplus;
     int vec;
 };
+
+// Step and reset mask of token l of a row (the first token after a segment), or
+// (0, 0) past the row end.
+template <typename T>
+__device__ __forceinline__ void token_step(const T* __restrict__ dr, const int32_t* __restrict__ pr,
+                                           int64_t l, int64_t L, float dbias, int softplus,
+                                           float& dt, float& m) {
+    dt = 0.0f;
+    m = 0.0f;
+    if (l < L) {
+        const float s = Storage<T>::load1(dr + l) + dbias;
+        dt = softplus ? softplus_f(s) : s;
+        m = pr[l] == 0 ? -INFINITY : 0.0f;
+    }
+}
 
 // Three waves per SIMD (at most 168 VGPRs): three blocks share a CU, so one block's
 // barrier waits are covered by the other two; measured faster than two waves
@@ -85,11 +109,15 @@ void scan_bwd_kernel(BwdParams p) {
     const int r = tid >> 4;
     const int64_t b = blockIdx.y;
     const int64_t g = blockIdx.x;
+    const int seg = blockIdx.z;
     const int64_t d_raw = g * kRows + r;
     const bool active = d_raw < p.dim;
     const int64_t d = active ? d_raw : p.dim - 1;
     const int64_t L = p.L;
     const int64_t rowoff = (b * p.dim + d) * L;
+    const int64_t nchunk = (L + kCH - 1) / kCH;
+    const int64_t c0 = (int64_t)seg * p.seg_chunks;
+    const int64_t c1 = min(nchunk, c0 + p.seg_chunks);
 
     const T* ur = static_cast<const T*>(p.u) + rowoff;
     const T* dr = static_cast<const T*>(p.delta) + rowoff;
@@ -102,20 +130,20 @@ void scan_bwd_kernel(BwdParams p) {
     const T* Cb = static_cast<const T*>(p.C) + b * kN * L;
     const int32_t* pr = p.pos + b * L;
 
-    {   // per-channel tables
-        const int rr = tid >> 4, n = tid & 15;
-        const int64_t dd = min((int64_t)g * kRows + rr, p.dim - 1);
-        sm.A2[rr][n] = p.A[dd * kN + n] * kLog2e;
-        sm.xc[rr][n] = 0.0f;
-        sm.an[rr][n] = 0.0f;
-        sm.dA[rr][n] = 0.0f;
-    }
     const float Dd = p.D ? p.D[d] : 0.0f;
     const float dbias = p.delta_bias ? p.delta_bias[d] : 0.0f;
     float dDacc = 0.0f, dbacc = 0.0f;
-    float dt_next = 0.0f, m_next = 0.0f;     // step and mask of the first token of the chunk to the right
-
-    const int64_t nchunk = (L + kCH - 1) / kCH;
+    float dt_next, m_next;     // step and mask of the first token of the chunk to the right
+    token_step<T>(dr, pr, c1 * kCH, L, dbias, p.softplus, dt_next, m_next);
+    {   // per-channel tables; every lane of row rr holds the same dt_next, m_next
+        const int rr = tid >> 4, n = tid & 15;
+        const int64_t dd = min((int64_t)g * kRows + rr, p.dim - 1);
+        const float A2n = p.A[dd * kN + n] * kLog2e;
+        sm.A2[rr][n] = A2n;
+        sm.xc[rr][n] = p.xc_in ? p.xc_in[((b * p.dim + dd) * p.nseg + seg) * kN + n] : 0.0f;
+        sm.an[rr][n] = c1 < nchunk ? fast_exp2(fmaf(dt_next, A2n, m_next)) : 0.0f;
+        sm.dA[rr][n] = 0.0f;
+    }
     // One chunk; FULL (block-uniform) means the chunk lies inside the row and vector
     // access is allowed, so every load and store is unconditional.
     auto chunk = [&](auto full_tag, const int64_t c) {
@@ -341,7 +369,7 @@ void scan_bwd_kernel(BwdParams p) {
         }
         __syncthreads();     // LDS is restaged for the next chunk
     };
-    for (int64_t c = nchunk - 1; c >= 0; --c) {
+    for (int64_t c = c1 - 1; c >= c0; --c) {
         if (p.vec && (c + 1) * kCH <= L) chunk(std::true_type{}, c);
         else chunk(std::false_type{}, c);
     }
@@ -349,15 +377,175 @@ void scan_bwd_kernel(BwdParams p) {
     // ---- per-channel partials ----
     dDacc = row_sum_to_15(dDacc);
     dbacc = row_sum_to_15(dbacc);
+    float* pcb = p.part_chan + (b * p.nseg + seg) * p.dim * (kN + 2);
     if (active && j == 15) {
-        float* pc = p.part_chan + (b * p.dim + d) * (kN + 2);
+        float* pc = pcb + d * (kN + 2);
         pc[kN] = dDacc;
         pc[kN + 1] = dbacc;
     }
     {
         const int rr = tid >> 4, n = tid & 15;
         if ((int64_t)g * kRows + rr < p.dim)
-            p.part_chan[(b * p.dim + g * kRows + rr) * (kN + 2) + n] = sm.dA[rr][n];
+            pcb[(g * kRows + rr) * (kN + 2) + n] = sm.dA[rr][n];
+    }
+}
+
+// Aggregate pass of one segment (blockIdx.z + 1; the first segment needs none): the
+// reverse recurrence over the segment with x = 0 gives H = dh at its first token,
+// and Q = the product of the multipliers Abar_{l+1} over its tokens l, so that
+// dh_first = Q x + H.  Same arithmetic as the main pass, without the forward replay
+// and the gradients.
+struct __attribute__((aligned(16))) AggSmem {
+    float C[kN][16][kSeg];
+    float M[16][kSeg];
+    float A2[kRows][kN];
+    float xc[kRows][kN];
+    float q[kRows][kN];
+};
+
+template <typename T>
+__global__ __launch_bounds__(kThreads) void scan_bwd_agg_kernel(BwdParams p) {
+    constexpr int PV = Storage<T>::kPerVec;
+    constexpr int K = kK;
+    __shared__ AggSmem sm;
+
+    const int tid = threadIdx.x;
+    const int j = tid & 15;
+    const int r = tid >> 4;
+    const int64_t b = blockIdx.y;
+    const int64_t g = blockIdx.x;
+    const int seg = blockIdx.z + 1;
+    const int64_t d = min(g * kRows + r, p.dim - 1);
+    const int64_t L = p.L;
+    const int64_t rowoff = (b * p.dim + d) * L;
+    const int64_t nchunk = (L + kCH - 1) / kCH;
+    const int64_t c0 = (int64_t)seg * p.seg_chunks;
+    const int64_t c1 = min(nchunk, c0 + p.seg_chunks);
+
+    const T* dr = static_cast<const T*>(p.delta) + rowoff;
+    const T* zr = p.z ? static_cast<const T*>(p.z) + rowoff : nullptr;
+    const T* gr = static_cast<const T*>(p.dout) + rowoff;
+    const T* Cb = static_cast<const T*>(p.C) + b * kN * L;
+    const int32_t* pr = p.pos + b * L;
+
+    const float dbias = p.delta_bias ? p.delta_bias[d] : 0.0f;
+    float dt_next, m_next;
+    token_step<T>(dr, pr, c1 * kCH, L, dbias, p.softplus, dt_next, m_next);
+    {
+        const int rr = tid >> 4, n = tid & 15;
+        const int64_t dd = min(g * kRows + rr, p.dim - 1);
+        sm.A2[rr][n] = p.A[dd * kN + n] * kLog2e;
+        sm.xc[rr][n] = 0.0f;
+        sm.q[rr][n] = 1.0f;
+    }
+
+    auto chunk = [&](auto full_tag, const int64_t c) {
+        constexpr bool FULL = decltype(full_tag)::value;
+        const int64_t lb = c * kCH;
+        for (int idx = tid * PV; idx < kN * kCH; idx += kThreads * PV) {
+            const int n = idx / kCH, t = idx - n * kCH;
+            float vc[PV];
+            load_run<T, PV, FULL>(Cb + (int64_t)n * L, lb + t, L, p.vec, vc);
+            float* dc = &sm.C[n][t / K][t % K];
+#pragma unroll
+            for (int i = 0; i < PV; ++i) dc[i] = vc[i];
+        }
+        for (int t = tid; t < kCH; t += kThreads) {
+            const int64_t l = lb + t;
+            sm.M[t / K][t % K] = ((FULL || l < L) && pr[l] == 0) ? -INFINITY : 0.0f;
+        }
+        __syncthreads();
+
+        const int64_t l0 = lb + (int64_t)j * K;
+        float dt[K], dyD[K], M[K];
+        float S = 0.0f, Mr = 0.0f;
+        {
+            float dl[K];
+            load_run<T, K, FULL>(dr, l0, L, p.vec, dl);
+            load_run<T, K, FULL>(gr, l0, L, p.vec, dyD);
+            if (zr) {
+                float zv[K];
+                load_run<T, K, FULL>(zr, l0, L, p.vec, zv);
+#pragma unroll
+                for (int k = 0; k < K; ++k) dyD[k] *= zv[k] * sigmoid_f(zv[k]);
+            }
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                const float s = dl[k] + dbias;
+                float v = s;
+                if (p.softplus) v = softplus_f(s);
+                if (!FULL) v = (l0 + k < L) ? v : 0.0f;
+                dt[k] = v;
+            }
+#pragma unroll
+            for (int k = 0; k < K; k += 4) {
+                const f32x4 m = *reinterpret_cast<const f32x4*>(&sm.M[j][k]);
+                M[k] = m.x; M[k + 1] = m.y; M[k + 2] = m.z; M[k + 3] = m.w;
+            }
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                S += dt[k];
+                if (k > 0) Mr += M[k];
+            }
+        }
+        const float dt0n = dpp<kRowShl1>(dt_next, dt[0]);
+        const float m0n = dpp<kRowShl1>(m_next, M[0]);
+        const float Sr = S - dt[0] + dt0n;
+        Mr += m0n;
+        dt_next = dpp<kNewBcast0>(0.0f, dt[0]);
+        m_next = dpp<kNewBcast0>(0.0f, M[0]);
+
+#pragma unroll 1
+        for (int n = 0; n < kN; ++n) {
+            const float A2n = sm.A2[r][n];
+            const float xc = sm.xc[r][n];
+            float cdy[K];
+#pragma unroll
+            for (int k = 0; k < K; k += 4) {
+                const f32x4 cv = *reinterpret_cast<const f32x4*>(&sm.C[n][j][k]);
+                cdy[k] = cv.x * dyD[k]; cdy[k + 1] = cv.y * dyD[k + 1];
+                cdy[k + 2] = cv.z * dyD[k + 2]; cdy[k + 3] = cv.w * dyD[k + 3];
+            }
+            float Hr = cdy[K - 1];
+#pragma unroll
+            for (int k = K - 2; k >= 0; --k)
+                Hr = fmaf(fast_exp2(fmaf(dt[k + 1], A2n, M[k + 1])), Hr, cdy[k]);
+            float Pr = fast_exp2(fmaf(Sr, A2n, Mr));
+            row_scan_down(Pr, Hr);
+            if (j == 0) {
+                sm.xc[r][n] = fmaf(Pr, xc, Hr);
+                sm.q[r][n] *= Pr;                 // lane 0's Pr spans the chunk
+            }
+        }
+        __syncthreads();
+    };
+    for (int64_t c = c1 - 1; c >= c0; --c) {
+        if (p.vec && (c + 1) * kCH <= L) chunk(std::true_type{}, c);
+        else chunk(std::false_type{}, c);
+    }
+    {
+        const int rr = tid >> 4, n = tid & 15;
+        const int64_t dd = g * kRows + rr;
+        if (dd < p.dim) {
+            float* o = p.agg + (((b * p.dim + dd) * p.nseg + seg) * kN + n) * 2;
+            o[0] = sm.q[rr][n];
+            o[1] = sm.xc[rr][n];
+        }
+    }
+}
+
+// Chains the segment maps from the row end: xc[s] = dh at the first token of segment s+1.
+__global__ void scan_bwd_carry_kernel(const float* __restrict__ agg, float* __restrict__ xc,
+                                      int64_t rows_n, int nseg) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;   // over batch*dim*kN
+    if (i >= rows_n) return;
+    const int64_t bd = i / kN;
+    const int n = (int)(i - bd * kN);
+    float x = 0.0f;
+    for (int s = nseg - 1; s >= 0; --s) {
+        const int64_t o = (bd * nseg + s) * kN + n;
+        xc[o] = x;
+        if (s > 0) x = fmaf(agg[2 * o], x, agg[2 * o + 1]);
     }
 }
 
@@ -390,16 +578,16 @@ __global__ void scan_bwd_finalize_bc(const float* __restrict__ part, float* __re
     *reinterpret_cast<f32x4*>(dst) = (acc[0] + acc[1]) + (acc[2] + acc[3]);
 }
 
-// dA[d,n], dD[d], ddelta_bias[d] = sum over batch rows (fixed order)
+// dA[d,n], dD[d], ddelta_bias[d] = sum over batch rows and segments (fixed order)
 __global__ void scan_bwd_finalize_chan(const float* __restrict__ part, float* __restrict__ dA,
                                        float* __restrict__ dD, float* __restrict__ ddb,
-                                       int64_t batch, int64_t dim) {
+                                       int64_t nparts, int64_t dim) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;   // over dim*(kN+2)
     if (i >= dim * (kN + 2)) return;
     const int64_t d = i / (kN + 2);
     const int q = (int)(i - d * (kN + 2));
     float s = 0.0f;
-    for (int64_t b = 0; b < batch; ++b) s += part[(b * dim + d) * (kN + 2) + q];
+    for (int64_t b = 0; b < nparts; ++b) s += part[(b * dim + d) * (kN + 2) + q];
     if (q < kN) dA[d * kN + q] = s;
     else if (q == kN) { if (dD) dD[d] = s; }
     else if (ddb) ddb[d] = s;
@@ -416,9 +604,28 @@ hipError_t launch_t(const ScanArgs& a, hipStream_t s) {
     p.groups = (int)((a.dim + kRows - 1) / kRows);
     p.softplus = a.softplus;
     p.vec = (a.seqlen % Storage<T>::kPerVec) == 0 && (a.seqlen % Storage<TO>::kPerVec) == 0;
-    dim3 grid((unsigned)p.groups, (unsigned)a.batch);
-    hipLaunchKernelGGL((scan_bwd_kernel<T, TO>), grid, dim3(kThreads), 0, s, p);
-    hipError_t e = hipGetLastError();
+    const SegPlan sp = scan_segments(a.batch, a.dim, a.seqlen);
+    static_assert(kSegUnit % kCH == 0, "segments hold whole chunks");
+    p.seg_chunks = sp.seg_len / kCH;
+    p.nseg = (int)sp.nseg;
+    p.agg = a.ws_agg;
+    p.xc_in = nullptr;
+    hipError_t e;
+    if (sp.nseg > 1) {
+        hipLaunchKernelGGL((scan_bwd_agg_kernel<T>), dim3((unsigned)p.groups, (unsigned)a.batch, (unsigned)(sp.nseg - 1)),
+                           dim3(kThreads), 0, s, p);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        const int64_t rows_n = a.batch * a.dim * kN;
+        hipLaunchKernelGGL(scan_bwd_carry_kernel, dim3((unsigned)((rows_n + 255) / 256)), dim3(256), 0, s,
+                           a.ws_agg, a.ws_carry, rows_n, p.nseg);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        p.xc_in = a.ws_carry;
+    }
+    hipLaunchKernelGGL((scan_bwd_kernel<T, TO>), dim3((unsigned)p.groups, (unsigned)a.batch, (unsigned)sp.nseg),
+                       dim3(kThreads), 0, s, p);
+    e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int64_t nbc4 = (a.batch * 2 * kN * a.seqlen + 3) / 4;
     hipLaunchKernelGGL(scan_bwd_finalize_bc, dim3((unsigned)((nbc4 + 255) / 256)), dim3(256), 0, s,
@@ -427,7 +634,7 @@ hipError_t launch_t(const ScanArgs& a, hipStream_t s) {
     if (e != hipSuccess) return e;
     const int64_t nch = a.dim * (kN + 2);
     hipLaunchKernelGGL(scan_bwd_finalize_chan, dim3((unsigned)((nch + 255) / 256)), dim3(256), 0, s,
-                       a.part_chan, a.dA, a.dD, a.ddelta_bias, a.batch, a.dim);
+                       a.part_chan, a.dA, a.dD, a.ddelta_bias, a.batch * sp.nseg, a.dim);
     return hipGetLastError();
 }
 

@@ -19,6 +19,10 @@
 //    a product range that contains a start is therefore 0 inside the fold and the
 //    scan alike (§3.4).
 //  - Tokens past the row end get dt = 0 and u = 0, i.e. the identity (1, 0).
+//  - Long rows with few channels are split into segments scanned by different
+//    blocks: an aggregate pass folds each segment into one map h -> P h + H per
+//    (channel, state), a carry pass chains the maps along the row, and the main
+//    pass starts each segment from its chained carry.
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -40,6 +44,7 @@ struct __attribute__((aligned(16))) FwdSmem {
     float M[16][kSeg];          // 0, or -inf on a sequence start
     float A2[kRows][kN];        // A * log2(e)
     float carry[kRows][kN];     // state after the previous chunk
+    float pseg[kRows][kN];      // aggregate pass: product of the multipliers so far
 };
 
 struct FwdParams {
@@ -54,13 +59,18 @@ struct FwdParams {
     const int32_t* pos;
     void* out;
     float* states;
+    float* agg;               // aggregate pass output: (batch, dim, nseg, kN, 2) = (P, H)
+    const float* carry_in;    // main pass: state before each segment (batch, dim, nseg, kN), or null
     int64_t dim, L;
+    int64_t seg_chunks;       // chunks per segment
+    int nseg;
     int nchunk_states;
     int softplus;
     int vec;
 };
 
-template <typename T, typename TO, int K>
+// AGG: aggregate pass over one segment (no C, no outputs), writes its map (P, H).
+template <typename T, typename TO, int K, bool AGG>
 __global__ __launch_bounds__(kThreads) void scan_fwd_kernel(FwdParams p) {
     constexpr int CH = 16 * K;
     constexpr int PV = Storage<T>::kPerVec;
@@ -71,6 +81,7 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_kernel(FwdParams p) {
     const int j = tid & 15;                       // lane position inside the row
     const int r = tid >> 4;                       // row (channel) inside the block
     const int64_t b = blockIdx.y;
+    const int seg = blockIdx.z;
     const int64_t d_raw = (int64_t)blockIdx.x * kRows + r;
     const bool active = d_raw < p.dim;
     const int64_t d = active ? d_raw : p.dim - 1;
@@ -89,7 +100,8 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_kernel(FwdParams p) {
         const int rr = tid >> 4, n = tid & 15;
         const int64_t dd = min((int64_t)blockIdx.x * kRows + rr, p.dim - 1);
         sm.A2[rr][n] = p.A[dd * kN + n] * kLog2e;
-        sm.carry[rr][n] = 0.0f;
+        sm.carry[rr][n] = (!AGG && p.carry_in) ? p.carry_in[((b * p.dim + dd) * p.nseg + seg) * kN + n] : 0.0f;
+        sm.pseg[rr][n] = 1.0f;
     }
     const float Dd = p.D ? p.D[d] : 0.0f;
     const float dbias = p.delta_bias ? p.delta_bias[d] : 0.0f;
@@ -105,11 +117,14 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_kernel(FwdParams p) {
             const int n = idx / CH, t = idx - n * CH;
             float vb[PV], vc[PV];
             load_run<T, PV, FULL>(Bb + (int64_t)n * L, lb + t, L, p.vec, vb);
-            load_run<T, PV, FULL>(Cb + (int64_t)n * L, lb + t, L, p.vec, vc);
+            if (!AGG) load_run<T, PV, FULL>(Cb + (int64_t)n * L, lb + t, L, p.vec, vc);
             float* db = &sm.B[n][t / K][t % K];
             float* dc = &sm.C[n][t / K][t % K];
 #pragma unroll
-            for (int q = 0; q < PV; ++q) { db[q] = vb[q]; dc[q] = vc[q]; }
+            for (int q = 0; q < PV; ++q) {
+                db[q] = vb[q];
+                if (!AGG) dc[q] = vc[q];
+            }
         }
         for (int t = tid; t < CH; t += kThreads) {
             const int64_t l = lb + t;
@@ -168,7 +183,11 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_kernel(FwdParams p) {
             row_scan_up(P, H);
             const float hend = fmaf(P, cin, H);               // state after this lane's last token
             float h = dpp<kRowShr1>(cin, hend);               // state before this lane's first token
-            if (j == 15) sm.carry[r][n] = hend;               // state after the chunk
+            if (j == 15) {
+                sm.carry[r][n] = hend;                        // state after the chunk
+                if (AGG) sm.pseg[r][n] *= P;                  // lane 15's P spans the chunk
+            }
+            if (AGG) continue;
 #pragma unroll
             for (int k = 0; k < K; k += 4) {
                 const f32x4 cv = *reinterpret_cast<const f32x4*>(&sm.C[n][j][k]);
@@ -188,7 +207,7 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_kernel(FwdParams p) {
         }
 
         // ---- gate and store ----
-        if (orow && active) {
+        if (!AGG && orow && active) {
             if (zr) {
                 float zv[K];
                 load_run<T, K, FULL>(zr, l0, L, p.vec, zv);
@@ -199,9 +218,36 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_kernel(FwdParams p) {
         }
         __syncthreads();      // LDS is restaged for the next chunk
     };
-    for (int64_t c = 0; c < nchunk; ++c) {
+    const int64_t c0 = (int64_t)seg * p.seg_chunks;
+    const int64_t c1 = min(nchunk, c0 + p.seg_chunks);
+    for (int64_t c = c0; c < c1; ++c) {
         if (p.vec && (c + 1) * CH <= L) chunk(std::true_type{}, c);
         else chunk(std::false_type{}, c);
+    }
+    if (AGG) {
+        __syncthreads();
+        const int rr = tid >> 4, n = tid & 15;
+        const int64_t dd = (int64_t)blockIdx.x * kRows + rr;
+        if (dd < p.dim) {
+            float* o = p.agg + (((b * p.dim + dd) * p.nseg + seg) * kN + n) * 2;
+            o[0] = sm.pseg[rr][n];
+            o[1] = sm.carry[rr][n];
+        }
+    }
+}
+
+// Chains the segment maps along each row: carry[s] = state after segment s-1.
+__global__ void scan_fwd_carry_kernel(const float* __restrict__ agg, float* __restrict__ carry,
+                                      int64_t rows_n, int nseg) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;   // over batch*dim*kN
+    if (i >= rows_n) return;
+    const int64_t bd = i / kN;
+    const int n = (int)(i - bd * kN);
+    float h = 0.0f;
+    for (int s = 0; s < nseg; ++s) {
+        const int64_t o = (bd * nseg + s) * kN + n;
+        carry[o] = h;
+        if (s + 1 < nseg) h = fmaf(agg[2 * o], h, agg[2 * o + 1]);
     }
 }
 
@@ -214,8 +260,28 @@ hipError_t launch_t(const ScanArgs& a, hipStream_t s) {
     p.nchunk_states = (int)((a.seqlen + kStride - 1) / kStride);
     p.softplus = a.softplus;
     p.vec = (a.seqlen % Storage<T>::kPerVec) == 0 && (a.seqlen % Storage<TO>::kPerVec) == 0;
-    dim3 grid((unsigned)((a.dim + kRows - 1) / kRows), (unsigned)a.batch);
-    hipLaunchKernelGGL((scan_fwd_kernel<T, TO, K>), grid, dim3(kThreads), 0, s, p);
+    const SegPlan sp = scan_segments(a.batch, a.dim, a.seqlen);
+    static_assert(kSegUnit % (16 * K) == 0, "segments hold whole chunks");
+    p.seg_chunks = sp.seg_len / (16 * K);
+    p.nseg = (int)sp.nseg;
+    p.agg = a.ws_agg;
+    p.carry_in = nullptr;
+    const unsigned groups = (unsigned)((a.dim + kRows - 1) / kRows);
+    if (sp.nseg > 1) {
+        // aggregate every segment but the last, then chain
+        hipLaunchKernelGGL((scan_fwd_kernel<T, TO, K, true>), dim3(groups, (unsigned)a.batch, (unsigned)(sp.nseg - 1)),
+                           dim3(kThreads), 0, s, p);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        const int64_t rows_n = a.batch * a.dim * kN;
+        hipLaunchKernelGGL(scan_fwd_carry_kernel, dim3((unsigned)((rows_n + 255) / 256)), dim3(256), 0, s,
+                           a.ws_agg, a.ws_carry, rows_n, p.nseg);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        p.carry_in = a.ws_carry;
+    }
+    hipLaunchKernelGGL((scan_fwd_kernel<T, TO, K, false>), dim3(groups, (unsigned)a.batch, (unsigned)sp.nseg),
+                       dim3(kThreads), 0, s, p);
     return hipGetLastError();
 }
 

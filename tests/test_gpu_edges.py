@@ -30,6 +30,33 @@ def test_ragged_shapes(shape, dtype):
     compare(r, oracle_run(d), TOL[dtype], ALL, label=f"{shape} {dtype} ")
 
 
+# Shapes with at least 768 blocks of 16 channels: the scans keep one segment per row
+# (every other small shape here is split into segments of 256 tokens or more).
+UNSPLIT = [(48, 256, 600), (52, 240, 1025)]
+
+
+@pytest.mark.parametrize("shape", UNSPLIT, ids=lambda s: "x".join(map(str, s)))
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_unsplit_rows(shape, dtype):
+    import paper_2408_03865_amd as P
+    assert P.segments(*shape) == 1
+    cfg = _cfg(*shape, dtype)
+    note(f"edge unsplit shape {shape} {dtype}")
+    d = W.make_inputs(cfg, variant="general")
+    r = run_gpu(gpu_inputs(d, dtype), out_f32=(dtype == "bf16"))
+    compare(r, oracle_run(d), TOL[dtype], ALL, label=f"{shape} {dtype} ")
+
+
+def test_split_shapes_are_split():
+    """The small shapes above do exercise the segment split, including a last
+    segment of a single token and one of 8 tokens."""
+    import paper_2408_03865_amd as P
+    assert P.segments(3, 5, 1000) == 4
+    assert P.segments(2, 33, 2049) == 9
+    assert P.segments(1, 3, 4104) == 17
+    assert P.segments(1, 16, 256) == 1
+
+
 OPTIONS = {
     "no-D": dict(D=None),
     "no-z": dict(z=None),
