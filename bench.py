@@ -8,7 +8,12 @@ the scan's du), over one batch of the Mamba-1.4B layer shape: 8 packed rows of
 state.  Inputs are resident in HBM before timing starts; every buffer, including
 the workspaces, is allocated beforehand.  Prints one JSON line.
 
-  python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2] [--no-cpu-baseline]
+At that shape the line also carries "comparison": the same real tokens through the
+same kernels padded to the longest sequence (one sequence per row) and run one
+sequence per call chain, with the packed path's speedup over each.
+
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2] [--variant paper|general]
+                  [--no-cpu-baseline] [--no-compare]
 """
 from __future__ import annotations
 
@@ -82,6 +87,133 @@ def cpu_baseline(d, cfg, rows):
             "seconds": dt}
 
 
+class Chain:
+    """Buffers and C-ABI calls of one step: conv fwd -> scan fwd (saving chunk states)
+    -> scan bwd -> conv bwd (upstream gradient = the scan's du).  Every buffer,
+    workspaces included, is allocated here, before any timing."""
+
+    def __init__(self, lib, t, code, width, stream):
+        import torch
+        from paper_2408_03865_amd import _lib
+        self.lib, self.t, self.code, self.W, self.sp = lib, t, code, width, stream.cuda_stream
+        x = t["x"]
+        self.Nb, self.Dn, self.L = x.shape
+        self.N = t["A"].shape[1]
+        Nb, Dn, L, N, dev = self.Nb, self.Dn, self.L, self.N, x.device
+        e = lambda: torch.empty_like(x)  # noqa: E731
+        self.u, self.out, self.du, self.ddl, self.dz, self.dx = (e() for _ in range(6))
+        self.dA, self.dD, self.ddb = (torch.empty_like(t[k]) for k in ("A", "D", "delta_bias"))
+        self.dB = torch.empty((Nb, N, L), dtype=torch.float32, device=dev)
+        self.dC = torch.empty_like(self.dB)
+        self.dw, self.dcb = torch.empty_like(t["w"]), torch.empty_like(t["bias"])
+        nst = (L + _lib.STATE_STRIDE - 1) // _lib.STATE_STRIDE
+        self.states = torch.empty((Nb, Dn, nst, N), dtype=torch.float32, device=dev)
+
+        def ws(n):
+            return torch.empty(max(1, int(n)), dtype=torch.uint8, device=dev)
+        self.ws_fwd = ws(lib.packmamba_selective_scan_fwd_workspace_size(Nb, Dn, L, N))
+        self.ws_scan = ws(lib.packmamba_selective_scan_bwd_workspace_size(Nb, Dn, L, N))
+        self.ws_conv = ws(lib.packmamba_causal_conv1d_bwd_workspace_size(Nb, Dn, L, width))
+
+    def ops(self):
+        from paper_2408_03865_amd import _lib
+        lib, t, c, sp = self.lib, self.t, self.code, self.sp
+        Nb, Dn, L, N, W = self.Nb, self.Dn, self.L, self.N, self.W
+        P = lambda v: v.data_ptr()  # noqa: E731
+
+        def conv_fwd():
+            _lib.check("conv_fwd", lib.packmamba_causal_conv1d_fwd(
+                P(t["x"]), P(t["w"]), P(t["bias"]), P(t["pos"]), P(self.u), Nb, Dn, L, W, c, 1, sp))
+
+        def scan_fwd():
+            _lib.check("scan_fwd", lib.packmamba_selective_scan_fwd(
+                P(self.u), P(t["delta"]), P(t["A"]), P(t["B"]), P(t["C"]), P(t["D"]), P(t["z"]),
+                P(t["delta_bias"]), 1, P(t["pos"]), P(self.out), P(self.states),
+                P(self.ws_fwd), self.ws_fwd.numel(), Nb, Dn, L, N, c, sp))
+
+        def scan_bwd():
+            _lib.check("scan_bwd", lib.packmamba_selective_scan_bwd(
+                P(self.u), P(t["delta"]), P(t["A"]), P(t["B"]), P(t["C"]), P(t["D"]), P(t["z"]),
+                P(t["delta_bias"]), 1, P(t["pos"]), P(t["dout"]), P(self.states),
+                P(self.du), P(self.ddl), P(self.dA), P(self.dB), P(self.dC), P(self.dD), P(self.dz),
+                P(self.ddb), P(self.ws_scan), self.ws_scan.numel(), Nb, Dn, L, N, c, sp))
+
+        def conv_bwd():
+            _lib.check("conv_bwd", lib.packmamba_causal_conv1d_bwd(
+                P(t["x"]), P(t["w"]), P(t["bias"]), P(t["pos"]), P(self.du), P(self.dx), P(self.dw),
+                P(self.dcb), P(self.ws_conv), self.ws_conv.numel(), Nb, Dn, L, W, c, 1, sp))
+
+        return [("conv_fwd", conv_fwd), ("scan_fwd", scan_fwd), ("scan_bwd", scan_bwd),
+                ("conv_bwd", conv_bwd)]
+
+
+def sequences(pos):
+    """(row, offset, length) of every packed sequence, from the position indices."""
+    import numpy as np
+    out = []
+    for b in range(pos.shape[0]):
+        st = np.flatnonzero(pos[b] == 0).tolist() + [pos.shape[1]]
+        out += [(b, st[i], st[i + 1] - st[i]) for i in range(len(st) - 1)]
+    return out
+
+
+def comparison(lib, tens, pos_host, code, width, stream, steps, warmup, packed_ms):
+    """The same real tokens and kernels without packing: (a) padded, one sequence per row
+    padded with zeros to the longest length, position indices 0..L-1 on every row; (b)
+    single, one call chain per sequence.  Tokens/s counts real tokens only."""
+    import torch
+    seqs = sequences(pos_host)
+    real = sum(n for _, _, n in seqs)
+    lmax = max(n for _, _, n in seqs)
+    dev = tens["x"].device
+
+    def timed(step_fn):
+        for _ in range(warmup):
+            step_fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(steps):
+            step_fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps
+
+    res = {"sequences": len(seqs), "real_tokens": real}
+    # (a) padded
+    pt = {k: tens[k] for k in ("A", "D", "delta_bias", "w", "bias")}
+    for k in ("x", "delta", "z", "B", "C", "dout"):
+        src = tens[k]
+        dst = torch.zeros((len(seqs), src.shape[1], lmax), dtype=src.dtype, device=dev)
+        for i, (b, o, n) in enumerate(seqs):
+            dst[i, :, :n] = src[b, :, o:o + n]
+        pt[k] = dst
+    pt["pos"] = torch.arange(lmax, dtype=torch.int32, device=dev).repeat(len(seqs), 1).contiguous()
+    ch = Chain(lib, pt, code, width, stream)
+    ops = [f for _, f in ch.ops()]
+    ms = timed(lambda: [f() for f in ops])
+    res["padded"] = {"rows": len(seqs), "seqlen": lmax, "ms_per_step": round(ms, 4),
+                     "tokens_per_s": round(real / (ms * 1e-3), 1),
+                     "padding_frac": round(1.0 - real / (len(seqs) * lmax), 4),
+                     "packed_speedup": round(ms / packed_ms, 3)}
+    del ch, ops, pt
+    torch.cuda.empty_cache()
+    # (b) single
+    chains = []
+    for b, o, n in seqs:
+        st = {k: tens[k] for k in ("A", "D", "delta_bias", "w", "bias")}
+        for k in ("x", "delta", "z", "B", "C", "dout"):
+            st[k] = tens[k][b:b + 1, :, o:o + n].contiguous()
+        st["pos"] = torch.arange(n, dtype=torch.int32, device=dev).reshape(1, n)
+        chains.append(Chain(lib, st, code, width, stream))
+    ops = [f for c in chains for _, f in c.ops()]
+    ms = timed(lambda: [f() for f in ops])
+    res["single"] = {"calls_per_step": len(ops), "ms_per_step": round(ms, 4),
+                     "tokens_per_s": round(real / (ms * 1e-3), 1),
+                     "packed_speedup": round(ms / packed_ms, 3)}
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -90,6 +222,8 @@ def main():
     ap.add_argument("--config", default="2")
     ap.add_argument("--variant", default="paper", choices=["paper", "general"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-compare", action="store_true",
+                    help="skip the padded / single-sequence runs of the same tokens (Mamba-1.4B shape only)")
     ap.add_argument("--cpu-rows", type=int, default=8)
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only copy BYTES with a plain device copy (calibrates HBM byte counters)")
@@ -136,45 +270,12 @@ def main():
     def f32(a):
         return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
 
-    x, dl, z, B, C, dout = (act(d[k]) for k in ("x", "delta", "z", "B", "C", "dout"))
-    A, D, dbias, w, bias = (f32(d[k]) for k in ("A", "D", "delta_bias", "w", "bias"))
-    pos = torch.from_numpy(d["pos"]).to(dev)
-    u = torch.empty_like(x)
-    out = torch.empty_like(x)
-    du, ddl, dz, dx = (torch.empty_like(x) for _ in range(4))
-    dA, dD, ddb = torch.empty_like(A), torch.empty_like(D), torch.empty_like(dbias)
-    dB = torch.empty((Nb, N, L), dtype=torch.float32, device=dev)
-    dC = torch.empty_like(dB)
-    dw, dcb = torch.empty_like(w), torch.empty_like(bias)
-    nst = (L + _lib.STATE_STRIDE - 1) // _lib.STATE_STRIDE
-    states = torch.empty((Nb, Dn, nst, N), dtype=torch.float32, device=dev)
-    ws_scan = torch.empty(lib.packmamba_selective_scan_bwd_workspace_size(Nb, Dn, L, N), dtype=torch.uint8, device=dev)
-    ws_fwd = torch.empty(max(1, lib.packmamba_selective_scan_fwd_workspace_size(Nb, Dn, L, N)), dtype=torch.uint8, device=dev)
-    ws_conv = torch.empty(lib.packmamba_causal_conv1d_bwd_workspace_size(Nb, Dn, L, Wd), dtype=torch.uint8, device=dev)
+    tens = {k: act(d[k]) for k in ("x", "delta", "z", "B", "C", "dout")}
+    tens.update({k: f32(d[k]) for k in ("A", "D", "delta_bias", "w", "bias")})
+    tens["pos"] = torch.from_numpy(d["pos"]).to(dev)
     stream = torch.cuda.current_stream(dev)
-    sp = stream.cuda_stream
-    P = lambda t: t.data_ptr()  # noqa: E731
-
-    def conv_fwd():
-        _lib.check("conv_fwd", lib.packmamba_causal_conv1d_fwd(P(x), P(w), P(bias), P(pos), P(u), Nb, Dn, L, Wd, code, 1, sp))
-
-    def scan_fwd():
-        _lib.check("scan_fwd", lib.packmamba_selective_scan_fwd(
-            P(u), P(dl), P(A), P(B), P(C), P(D), P(z), P(dbias), 1, P(pos), P(out), P(states),
-            P(ws_fwd), ws_fwd.numel(), Nb, Dn, L, N, code, sp))
-
-    def scan_bwd():
-        _lib.check("scan_bwd", lib.packmamba_selective_scan_bwd(
-            P(u), P(dl), P(A), P(B), P(C), P(D), P(z), P(dbias), 1, P(pos), P(dout), P(states),
-            P(du), P(ddl), P(dA), P(dB), P(dC), P(dD), P(dz), P(ddb), P(ws_scan), ws_scan.numel(),
-            Nb, Dn, L, N, code, sp))
-
-    def conv_bwd():
-        _lib.check("conv_bwd", lib.packmamba_causal_conv1d_bwd(
-            P(x), P(w), P(bias), P(pos), P(du), P(dx), P(dw), P(dcb), P(ws_conv), ws_conv.numel(),
-            Nb, Dn, L, Wd, code, 1, sp))
-
-    ops = [("conv_fwd", conv_fwd), ("scan_fwd", scan_fwd), ("scan_bwd", scan_bwd), ("conv_bwd", conv_bwd)]
+    chain = Chain(lib, tens, code, Wd, stream)
+    ops = chain.ops()
 
     def step():
         for _, f in ops:
@@ -248,6 +349,10 @@ def main():
         "roofline": roof,
         "device": torch.cuda.get_device_name(0),
     }
+    if args.config == "2" and not args.no_compare:
+        print("# comparison: padded and single-sequence runs of the same tokens", file=sys.stderr, flush=True)
+        line["comparison"] = comparison(lib, tens, d["pos"], code, Wd, stream, steps=5, warmup=2,
+                                        packed_ms=ms_step)
     if not args.no_cpu_baseline:
         print("# cpu baseline (oracle)", file=sys.stderr, flush=True)
         line["cpu_baseline"] = cpu_baseline(d, cfg, args.cpu_rows)

@@ -401,6 +401,7 @@ struct __attribute__((aligned(16))) AggSmem {
     float A2[kRows][kN];
     float xc[kRows][kN];
     float q[kRows][kN];
+    int first_start;
 };
 
 template <typename T>
@@ -420,13 +421,43 @@ __global__ __launch_bounds__(kThreads) void scan_bwd_agg_kernel(BwdParams p) {
     const int64_t rowoff = (b * p.dim + d) * L;
     const int64_t nchunk = (L + kCH - 1) / kCH;
     const int64_t c0 = (int64_t)seg * p.seg_chunks;
-    const int64_t c1 = min(nchunk, c0 + p.seg_chunks);
+    int64_t c1 = min(nchunk, c0 + p.seg_chunks);
 
     const T* dr = static_cast<const T*>(p.delta) + rowoff;
     const T* zr = p.z ? static_cast<const T*>(p.z) + rowoff : nullptr;
     const T* gr = static_cast<const T*>(p.dout) + rowoff;
     const T* Cb = static_cast<const T*>(p.C) + b * kN * L;
     const int32_t* pr = p.pos + b * L;
+
+    // dh at the segment's first token does not depend on the tokens from the first
+    // sequence start after it on (the multiplier into that start is 0), so the
+    // aggregate ends at the chunk holding the token before that start.
+    {
+        const int64_t ls = c0 * kCH;
+        const int64_t le = min(c1 * kCH, L);
+        const int64_t st = (le - 1) - (int64_t)pr[le - 1];
+        if (st > ls) {                       // some start lies in (ls, le): find the first
+            constexpr int kNone = 0x7fffffff;
+            if (tid == 0) sm.first_start = kNone;
+            __syncthreads();
+            for (int64_t base = ls + 1; base < le; base += kThreads * 4) {
+                int found = kNone;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const int64_t l = base + tid * 4 + k;
+                    if (l < le && found == kNone && pr[l] == 0) found = (int)l;
+                }
+                if (found != kNone) atomicMin(&sm.first_start, found);
+                __syncthreads();
+                const int v = sm.first_start;
+                __syncthreads();                 // every thread has read v before any new atomic
+                if (v != kNone) {
+                    c1 = min(c1, (int64_t)(v - 1) / kCH + 1);
+                    break;
+                }
+            }
+        }
+    }
 
     const float dbias = p.delta_bias ? p.delta_bias[d] : 0.0f;
     float dt_next, m_next;

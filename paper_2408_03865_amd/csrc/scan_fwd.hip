@@ -220,7 +220,15 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_kernel(FwdParams p) {
     };
     const int64_t c0 = (int64_t)seg * p.seg_chunks;
     const int64_t c1 = min(nchunk, c0 + p.seg_chunks);
-    for (int64_t c = c0; c < c1; ++c) {
+    int64_t cs = c0;
+    if (AGG) {
+        // The segment's map is unchanged by the chunks before the last sequence start
+        // inside it (that start's multiplier is 0), so the aggregate begins there.
+        const int64_t le = min(c1 * CH, L) - 1;
+        const int64_t st = le - (int64_t)pr[le];      // start of the sequence holding token le
+        if (st > c0 * CH) cs = min(st / CH, c1 - 1);
+    }
+    for (int64_t c = cs; c < c1; ++c) {
         if (p.vec && (c + 1) * CH <= L) chunk(std::true_type{}, c);
         else chunk(std::false_type{}, c);
     }

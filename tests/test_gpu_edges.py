@@ -57,6 +57,29 @@ def test_split_shapes_are_split():
     assert P.segments(1, 16, 256) == 1
 
 
+def _starts_to_lengths(starts, seqlen):
+    st = sorted(set(starts) | {0})
+    return [b - a for a, b in zip(st, st[1:] + [seqlen])]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_starts_on_segment_edges(dtype):
+    """A split row (8 segments of 256 tokens, backward chunks of 128) with sequence
+    starts exactly on a segment edge, one token after a segment start, on a backward
+    chunk edge inside a segment, on the last and first tokens of adjacent segments,
+    and a segment with no start at all."""
+    import paper_2408_03865_amd as P
+    shape = (1, 48, 2048)
+    assert P.segments(*shape) == 8
+    cfg = _cfg(*shape, dtype)
+    d = W.make_inputs(cfg, variant="general")
+    starts = [256, 513, 896, 1279, 1280, 1800, 2047]
+    d["pos"] = W.positions_from_lengths([_starts_to_lengths(starts, shape[2])], shape[2])
+    assert all(d["pos"][0, s] == 0 for s in starts)
+    r = run_gpu(gpu_inputs(d, dtype), out_f32=(dtype == "bf16"))
+    compare(r, oracle_run(d), TOL[dtype], ALL, label=f"segment edges {dtype} ")
+
+
 OPTIONS = {
     "no-D": dict(D=None),
     "no-z": dict(z=None),
