@@ -179,6 +179,21 @@ __device__ __forceinline__ void row_scan_down(float& P, float& H) {
     fmac_shl8(H, P); mul_shl8(P);
     dpp_tail_nop(P);
 }
+// Both scans at once: the forward scan of (P, H) and the reverse scan of (Pr, Hr),
+// interleaved so that every DPP read comes at least three instructions after the
+// write of its source.  No wait states are needed inside, and each chain hides
+// the other's DPP latency.
+#define PM_UD_LEVEL(N)                                                        \
+    "v_fmac_f32_dpp %1, %1, %0 row_shr:" #N " row_mask:0xf bank_mask:0xf\n\t" \
+    "v_fmac_f32_dpp %3, %3, %2 row_shl:" #N " row_mask:0xf bank_mask:0xf\n\t" \
+    "v_mul_f32_dpp %0, %0, %0 row_shr:" #N " row_mask:0xf bank_mask:0xf\n\t"  \
+    "v_mul_f32_dpp %2, %2, %2 row_shl:" #N " row_mask:0xf bank_mask:0xf\n\t"
+__device__ __forceinline__ void row_scan_up_down(float& P, float& H, float& Pr, float& Hr) {
+    asm("s_nop 1\n\t" PM_UD_LEVEL(1) PM_UD_LEVEL(2) PM_UD_LEVEL(4) PM_UD_LEVEL(8) "s_nop 1"
+        : "+v"(P), "+v"(H), "+v"(Pr), "+v"(Hr));
+}
+#undef PM_UD_LEVEL
+
 // Sum over the 16 lanes of a row, delivered to lane 15.
 __device__ __forceinline__ float row_sum_to_15(float x) {
     add_shr1(x); add_shr2(x); add_shr4(x); add_shr8(x);

@@ -240,22 +240,32 @@ void scan_bwd_kernel(BwdParams p) {
                 const f32x4 m = *reinterpret_cast<const f32x4*>(&sm.M[j][k]);
                 M[k] = m.x; M[k + 1] = m.y; M[k + 2] = m.z; M[k + 3] = m.w;
             }
-            // ---- replay the forward inside the chunk ----
+            // ---- fold the lane's tokens both ways, then both row scans at once ----
 #pragma unroll
             for (int k = 0; k < K; k += 4) {
                 const f32x4 v = *reinterpret_cast<const f32x4*>(&sm.B[n][j][k]);
                 bv[k] = v.x; bv[k + 1] = v.y; bv[k + 2] = v.z; bv[k + 3] = v.w;
+                const f32x4 cv = *reinterpret_cast<const f32x4*>(&sm.C[n][j][k]);
+                cdy[k] = cv.x * dyD[k]; cdy[k + 1] = cv.y * dyD[k + 1];
+                cdy[k + 2] = cv.z * dyD[k + 2]; cdy[k + 3] = cv.w * dyD[k + 3];
             }
 #pragma unroll
             for (int k = 0; k < K; ++k) {
                 a[k] = fast_exp2(fmaf(dt[k], A2n, M[k]));
                 bx[k] = dlu[k] * bv[k];
             }
+            // forward: h -> P h + H over the lane's tokens
             float H = bx[0];
 #pragma unroll
             for (int k = 1; k < K; ++k) H = fmaf(a[k], H, bx[k]);
+            // reverse: dh_l = Abar_{l+1} dh_{l+1} + C_l dy_l over the lane's tokens
+            float Hr = cdy[K - 1];
+#pragma unroll
+            for (int k = K - 2; k >= 0; --k) Hr = fmaf(a[k + 1], Hr, cdy[k]);
             float P = fast_exp2(fmaf(S, A2n, Mf));
-            row_scan_up(P, H);
+            float Pr = fast_exp2(fmaf(Sr, A2n, Mr));
+            row_scan_up_down(P, H, Pr, Hr);
+            // ---- replay the forward inside the chunk ----
             const float hend = fmaf(P, hin, H);
             float hprev = dpp<kRowShr1>(hin, hend);
 #pragma unroll
@@ -269,17 +279,11 @@ void scan_bwd_kernel(BwdParams p) {
                     const float h = ah[kk] + bx[kk];
                     yacc[kk] = fmaf(cc[q], h, yacc[kk]);
                     bx[kk] = dyD[kk] * h;                    // dC contribution (reuses bx)
-                    cdy[kk] = cc[q] * dyD[kk];
                     hprev = h;
                 }
             }
-            // ---- reverse recurrence: dh_l = Abar_{l+1} dh_{l+1} + C_l dy_l ----
+            // ---- reverse recurrence, entering with the carry from the right ----
             const float alast = dpp<kRowShl1>(an, a[0]);        // Abar of the next lane's first token
-            float Hr = cdy[K - 1];
-#pragma unroll
-            for (int k = K - 2; k >= 0; --k) Hr = fmaf(a[k + 1], Hr, cdy[k]);
-            float Pr = fast_exp2(fmaf(Sr, A2n, Mr));
-            row_scan_down(Pr, Hr);
             const float dhfirst = fmaf(Pr, xc, Hr);            // dh at this lane's first token
             float dh = dpp<kRowShl1>(xc, dhfirst);               // dh at the next lane's first token
             if (j == 0) {
