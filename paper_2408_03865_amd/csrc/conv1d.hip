@@ -15,19 +15,23 @@
 namespace pm {
 namespace {
 
-constexpr int kTok = 8;        // tokens per thread per step
+constexpr int kTok = 8;        // tokens per thread per step (forward), and the halo vector
+constexpr int kTokBwd = 8;     // tokens per thread per step (backward)
 constexpr int kThreads = 256;
 
+// N position indices from l0 (N a multiple of 4); beyond L they read 0
+template <int N = kTok>
 __device__ __forceinline__ void load_pos(const int32_t* __restrict__ pr, int64_t l0, int64_t L,
                                          bool pvec, int* p) {
-    if (pvec && l0 + kTok <= L) {
-        const u32x4 a = *reinterpret_cast<const u32x4*>(pr + l0);
-        const u32x4 b = *reinterpret_cast<const u32x4*>(pr + l0 + 4);
-        p[0] = (int)a.x; p[1] = (int)a.y; p[2] = (int)a.z; p[3] = (int)a.w;
-        p[4] = (int)b.x; p[5] = (int)b.y; p[6] = (int)b.z; p[7] = (int)b.w;
+    if (pvec && l0 + N <= L) {
+#pragma unroll
+        for (int i = 0; i < N; i += 4) {
+            const u32x4 a = *reinterpret_cast<const u32x4*>(pr + l0 + i);
+            p[i] = (int)a.x; p[i + 1] = (int)a.y; p[i + 2] = (int)a.z; p[i + 3] = (int)a.w;
+        }
     } else {
 #pragma unroll
-        for (int i = 0; i < kTok; ++i) p[i] = (l0 + i < L) ? pr[l0 + i] : 0;
+        for (int i = 0; i < N; ++i) p[i] = (l0 + i < L) ? pr[l0 + i] : 0;
     }
 }
 
@@ -101,7 +105,9 @@ __device__ __forceinline__ void block_sum(float* v, float* lds /* NV * (kThreads
     }
 }
 
-template <typename T, typename TO, int W>
+// Backward: each thread owns KT consecutive tokens per step and also recomputes
+// the activation gradient of the next W-1 tokens (the reverse-index halo).
+template <typename T, typename TO, int W, int KT>
 __global__ __launch_bounds__(kThreads) void conv1d_bwd_kernel(
     const T* __restrict__ x, const float* __restrict__ w, const float* __restrict__ bias,
     const int32_t* __restrict__ pos, const T* __restrict__ dout, TO* __restrict__ dx,
@@ -121,52 +127,53 @@ __global__ __launch_bounds__(kThreads) void conv1d_bwd_kernel(
 #pragma unroll
     for (int j = 0; j <= W; ++j) acc[j] = 0.0f;
 
-    for (int64_t l0 = (int64_t)threadIdx.x * kTok; l0 < L; l0 += (int64_t)kThreads * kTok) {
-        // x for tokens l0-8 .. l0+15 (pre-activations of this vector and the next W-1 tokens)
-        float xs[3 * kTok];
+    for (int64_t l0 = (int64_t)threadIdx.x * KT; l0 < L; l0 += (int64_t)kThreads * KT) {
+        // x for tokens l0-8 .. l0+KT+7 (pre-activations of this run and the next W-1 tokens)
+        float xs[kTok + KT + kTok];
         if (l0 > 0) load_run<T, kTok>(xr, l0 - kTok, L, vec, xs);
         else {
 #pragma unroll
             for (int i = 0; i < kTok; ++i) xs[i] = 0.0f;
         }
-        load_run<T, kTok>(xr, l0, L, vec, xs + kTok);
-        load_run<T, kTok>(xr, l0 + kTok, L, vec, xs + 2 * kTok);
-        float gs[2 * kTok];
-        load_run<T, kTok>(gr, l0, L, vec, gs);
-        load_run<T, kTok>(gr, l0 + kTok, L, vec, gs + kTok);
-        int p[2 * kTok];
-        load_pos(pr, l0, L, pvec, p);
-        load_pos(pr, l0 + kTok, L, pvec, p + kTok);
-        // g = dout * d out / d pre for tokens l0 .. l0+kTok+W-2 (zero beyond L: dout reads 0)
-        float g[kTok + W - 1];
+        load_run<T, KT>(xr, l0, L, vec, xs + kTok);
+        load_run<T, kTok>(xr, l0 + KT, L, vec, xs + kTok + KT);
+        float gs[KT + kTok];
+        load_run<T, KT>(gr, l0, L, vec, gs);
+        load_run<T, kTok>(gr, l0 + KT, L, vec, gs + KT);
+        int p[KT + kTok];
+        load_pos<KT>(pr, l0, L, pvec, p);
+        load_pos<kTok>(pr, l0 + KT, L, pvec, p + KT);
+        // gm[k][t] = g[t] if tap k of token t is live (k <= pos[t]) else 0, for tokens
+        // l0 .. l0+KT+W-2, g = dout * d out / d pre (0 beyond L: dout reads 0).  The
+        // same masked values give dx through the reverse indices (tap k of token j
+        // is live iff pos[j+k] >= k) and dw.
+        float gm[W][KT + W - 1];
 #pragma unroll
-        for (int t = 0; t < kTok + W - 1; ++t) {
+        for (int t = 0; t < KT + W - 1; ++t) {
             float gt = gs[t];
             if (silu) {
                 const float v = conv_pre<W>(xs, t, p[t], wk, b0);
                 const float s = sigmoid_f(v);
                 gt *= s * (1.0f + v * (1.0f - s));
             }
-            g[t] = gt;
+#pragma unroll
+            for (int k = 0; k < W; ++k) gm[k][t] = (k <= p[t]) ? gt : 0.0f;
         }
-        // dx through the reverse indices: tap k of token j+k is live iff pos[j+k] >= k
-        float o[kTok];
+        float o[KT];
 #pragma unroll
-        for (int i = 0; i < kTok; ++i) {
-            float a = 0.0f;
+        for (int i = 0; i < KT; ++i) {
+            float a = wk[W - 1] * gm[0][i];
 #pragma unroll
-            for (int k = 0; k < W; ++k)
-                if (p[i + k] >= k) a = fmaf(wk[W - 1 - k], g[i + k], a);
+            for (int k = 1; k < W; ++k) a = fmaf(wk[W - 1 - k], gm[k][i + k], a);
             o[i] = a;
         }
-        store_run<TO, kTok>(dxr, l0, L, vec, o);
+        store_run<TO, KT>(dxr, l0, L, vec, o);
         // parameter gradients from this thread's own tokens
 #pragma unroll
-        for (int i = 0; i < kTok; ++i) {
+        for (int i = 0; i < KT; ++i) {
 #pragma unroll
-            for (int k = 0; k < W; ++k)
-                if (k <= p[i]) acc[W - 1 - k] = fmaf(g[i], xs[kTok + i - k], acc[W - 1 - k]);
-            acc[W] += g[i];
+            for (int k = 0; k < W; ++k) acc[W - 1 - k] = fmaf(gm[k][i], xs[kTok + i - k], acc[W - 1 - k]);
+            acc[W] += gm[0][i];
         }
     }
     block_sum<W + 1>(acc, red);
@@ -213,9 +220,9 @@ hipError_t conv_bwd_t(const ConvArgs& a, hipStream_t s) {
     const T* g = static_cast<const T*>(a.dout);
     TO* dx = static_cast<TO*>(a.out);
     switch (a.width) {
-        case 2: hipLaunchKernelGGL((conv1d_bwd_kernel<T, TO, 2>), grid, block, 0, s, x, a.w, a.bias, a.pos, g, dx, a.partial, a.dim, a.seqlen, a.silu, vec, pvec); break;
-        case 3: hipLaunchKernelGGL((conv1d_bwd_kernel<T, TO, 3>), grid, block, 0, s, x, a.w, a.bias, a.pos, g, dx, a.partial, a.dim, a.seqlen, a.silu, vec, pvec); break;
-        default: hipLaunchKernelGGL((conv1d_bwd_kernel<T, TO, 4>), grid, block, 0, s, x, a.w, a.bias, a.pos, g, dx, a.partial, a.dim, a.seqlen, a.silu, vec, pvec); break;
+        case 2: hipLaunchKernelGGL((conv1d_bwd_kernel<T, TO, 2, kTokBwd>), grid, block, 0, s, x, a.w, a.bias, a.pos, g, dx, a.partial, a.dim, a.seqlen, a.silu, vec, pvec); break;
+        case 3: hipLaunchKernelGGL((conv1d_bwd_kernel<T, TO, 3, kTokBwd>), grid, block, 0, s, x, a.w, a.bias, a.pos, g, dx, a.partial, a.dim, a.seqlen, a.silu, vec, pvec); break;
+        default: hipLaunchKernelGGL((conv1d_bwd_kernel<T, TO, 4, kTokBwd>), grid, block, 0, s, x, a.w, a.bias, a.pos, g, dx, a.partial, a.dim, a.seqlen, a.silu, vec, pvec); break;
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
