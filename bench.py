@@ -35,7 +35,7 @@ VALU_PEAK = 256 * 4 * 16 * 2.4e9
 SLOTS_FWD = 6                  # Abar (mul + exp2), dt*B*u (mul), h (fma), y (fma)
 SLOTS_BWD = 17                 # replay Abar, Bbar x, h; dh (mul + fma); sum dh B (fma);
 #                                q = dh * Abar h_prev (2 mul); ddt (fma); dA (fma); dB, dC (mul + add each)
-KERNEL_SOURCES = ("common.hpp", "scan_bwd.hip")
+KERNEL_SOURCES = ("common.hpp", "launch.hpp", "scan_bwd.hip")
 
 
 def minimal_bytes(Nb, Dn, L, N, W, s):

@@ -224,17 +224,6 @@ __device__ __forceinline__ float softplus_f(float s) {
 }
 __device__ __forceinline__ float sigmoid_f(float v) { return fast_rcp(1.0f + fast_exp2(-v * kLog2e)); }
 
-// softplus(s) and its derivative sigmoid(s) = e / (1 + e), e = exp(s), sharing e;
-// above 20 softplus is the identity and its derivative 1.
-__device__ __forceinline__ void softplus_grad_f(float s, float& sp, float& gs) {
-    const float e = fast_exp2(s * kLog2e);
-    const float u = 1.0f + e;
-    const float d = u - 1.0f;
-    const float l1p = d == 0.0f ? e : kLn2 * fast_log2(u) * (e * fast_rcp(d));
-    sp = s > 20.0f ? s : l1p;
-    gs = s > 20.0f ? 1.0f : e * fast_rcp(u);
-}
-
 // Flat wave lane id and the lane's position inside its 16-lane row.
 __device__ __forceinline__ int lane_id() { return (int)(threadIdx.x & 63); }
 
