@@ -11,6 +11,10 @@ Functions and the passages they follow:
                               (A-bar forced to 0 where the position index is 0)
   scan_states              -- h at the end of every ``stride``-token chunk
   check_positions          -- the position-index contract of §3.1
+Each operator optionally takes and returns per-row states for a sequence cut at
+a row end and continued in another row (the future work of §5): the conv's width-1
+inputs before the row / the row's last width-1 inputs, the scan's h before the
+row / after it, with their gradients.
 """
 from __future__ import annotations
 
@@ -46,12 +50,12 @@ def load(path: Optional[str] = None):
         build(out=p)
     lib = ctypes.CDLL(p)
     dp, ip, i64, i32 = ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
-    lib.pmo_conv1d_fwd.argtypes = [dp, dp, dp, ip, dp, i64, i64, i64, i32, i32]
-    lib.pmo_conv1d_bwd.argtypes = [dp, dp, dp, ip, dp, dp, dp, dp, i64, i64, i64, i32, i32]
-    lib.pmo_scan_fwd.argtypes = [dp] * 8 + [i32, ip, dp, i64, i64, i64, i32]
-    lib.pmo_scan_states.argtypes = [dp, dp, dp, dp, dp, i32, ip, dp, i64, i64, i64, i32, i64]
-    lib.pmo_scan_bwd.argtypes = [dp] * 8 + [i32, ip, dp] + [dp] * 8 + [i64, i64, i64, i32]
-    lib.pmo_check_positions.argtypes = [ip, i64, i64]
+    lib.pmo_conv1d_fwd.argtypes = [dp, dp, dp, ip, dp, dp, dp, i64, i64, i64, i32, i32]
+    lib.pmo_conv1d_bwd.argtypes = [dp, dp, dp, ip] + [dp] * 7 + [i64, i64, i64, i32, i32]
+    lib.pmo_scan_fwd.argtypes = [dp] * 8 + [i32, ip, dp, dp, dp, i64, i64, i64, i32]
+    lib.pmo_scan_states.argtypes = [dp, dp, dp, dp, dp, i32, ip, dp, dp, i64, i64, i64, i32, i64]
+    lib.pmo_scan_bwd.argtypes = [dp] * 8 + [i32, ip] + [dp] * 12 + [i64, i64, i64, i32]
+    lib.pmo_check_positions.argtypes = [ip, i64, i64, i32]
     lib.pmo_check_positions.restype = i64
     lib.pmo_num_threads.restype = i32
     lib.pmo_set_num_threads.argtypes = [i32]
@@ -86,60 +90,69 @@ def set_num_threads(n: int, lib=None) -> None:
     (lib or load()).pmo_set_num_threads(int(n))
 
 
-def conv1d_fwd(x, w, bias, pos, silu=True, lib=None) -> np.ndarray:
+def conv1d_fwd(x, w, bias, pos, silu=True, lib=None, xinit=None, return_final=False):
+    """out, or (out, xfinal) with ``return_final``; xinit/xfinal are (batch, dim, width-1)."""
     lib = lib or load()
-    x, w, bias, pos = _f64(x), _f64(w), _f64(bias), _i32(pos)
+    x, w, bias, pos, xinit = _f64(x), _f64(w), _f64(bias), _i32(pos), _f64(xinit)
     Nb, Dn, L = x.shape
     W = w.shape[1]
     out = np.empty_like(x)
-    lib.pmo_conv1d_fwd(_ptr(x), _ptr(w), _ptr(bias), _ptr(pos), _ptr(out), Nb, Dn, L, W, int(silu))
-    return out
+    xfinal = np.empty((Nb, Dn, W - 1)) if return_final else None
+    lib.pmo_conv1d_fwd(_ptr(x), _ptr(w), _ptr(bias), _ptr(pos), _ptr(xinit), _ptr(out), _ptr(xfinal),
+                       Nb, Dn, L, W, int(silu))
+    return (out, xfinal) if return_final else out
 
 
-def conv1d_bwd(x, w, bias, pos, dout, silu=True, lib=None) -> Dict[str, np.ndarray]:
+def conv1d_bwd(x, w, bias, pos, dout, silu=True, lib=None, xinit=None, dxfinal=None) -> Dict[str, np.ndarray]:
     lib = lib or load()
     x, w, bias, pos, dout = _f64(x), _f64(w), _f64(bias), _i32(pos), _f64(dout)
+    xinit, dxfinal = _f64(xinit), _f64(dxfinal)
     Nb, Dn, L = x.shape
     W = w.shape[1]
     dx = np.empty_like(x)
     dw = np.empty_like(w)
     dbias = np.empty(Dn) if bias is not None else None
-    lib.pmo_conv1d_bwd(_ptr(x), _ptr(w), _ptr(bias), _ptr(pos), _ptr(dout), _ptr(dx), _ptr(dw),
-                       _ptr(dbias), Nb, Dn, L, W, int(silu))
-    return {"dx": dx, "dw": dw, "dbias": dbias}
+    dxinit = np.empty((Nb, Dn, W - 1)) if xinit is not None else None
+    lib.pmo_conv1d_bwd(_ptr(x), _ptr(w), _ptr(bias), _ptr(pos), _ptr(xinit), _ptr(dout), _ptr(dxfinal),
+                       _ptr(dx), _ptr(dw), _ptr(dbias), _ptr(dxinit), Nb, Dn, L, W, int(silu))
+    return {"dx": dx, "dw": dw, "dbias": dbias, "dxinit": dxinit}
 
 
 def scan_fwd(u, delta, A, B, C, D=None, z=None, delta_bias=None, delta_softplus=True, pos=None,
-             lib=None) -> np.ndarray:
+             lib=None, h0=None, return_final=False):
+    """out, or (out, hfinal) with ``return_final``; h0/hfinal are (batch, dim, dstate)."""
     lib = lib or load()
-    u, delta, A, B, C, D, z, delta_bias = map(_f64, (u, delta, A, B, C, D, z, delta_bias))
+    u, delta, A, B, C, D, z, delta_bias, h0 = map(_f64, (u, delta, A, B, C, D, z, delta_bias, h0))
     pos = _i32(pos)
     Nb, Dn, L = u.shape
     N = A.shape[1]
     out = np.empty_like(u)
+    hfinal = np.empty((Nb, Dn, N)) if return_final else None
     lib.pmo_scan_fwd(_ptr(u), _ptr(delta), _ptr(A), _ptr(B), _ptr(C), _ptr(D), _ptr(z),
-                     _ptr(delta_bias), int(delta_softplus), _ptr(pos), _ptr(out), Nb, Dn, L, N)
-    return out
+                     _ptr(delta_bias), int(delta_softplus), _ptr(pos), _ptr(h0), _ptr(out), _ptr(hfinal),
+                     Nb, Dn, L, N)
+    return (out, hfinal) if return_final else out
 
 
 def scan_states(u, delta, A, B, delta_bias=None, delta_softplus=True, pos=None, stride=128,
-                lib=None) -> np.ndarray:
+                lib=None, h0=None) -> np.ndarray:
     lib = lib or load()
-    u, delta, A, B, delta_bias = map(_f64, (u, delta, A, B, delta_bias))
+    u, delta, A, B, delta_bias, h0 = map(_f64, (u, delta, A, B, delta_bias, h0))
     pos = _i32(pos)
     Nb, Dn, L = u.shape
     N = A.shape[1]
     nchunk = (L + stride - 1) // stride
     st = np.empty((Nb, Dn, nchunk, N))
     lib.pmo_scan_states(_ptr(u), _ptr(delta), _ptr(A), _ptr(B), _ptr(delta_bias),
-                        int(delta_softplus), _ptr(pos), _ptr(st), Nb, Dn, L, N, stride)
+                        int(delta_softplus), _ptr(pos), _ptr(h0), _ptr(st), Nb, Dn, L, N, stride)
     return st
 
 
 def scan_bwd(u, delta, A, B, C, D=None, z=None, delta_bias=None, delta_softplus=True, pos=None,
-             dout=None, lib=None) -> Dict[str, np.ndarray]:
+             dout=None, lib=None, h0=None, dhfinal=None) -> Dict[str, np.ndarray]:
     lib = lib or load()
     u, delta, A, B, C, D, z, delta_bias, dout = map(_f64, (u, delta, A, B, C, D, z, delta_bias, dout))
+    h0, dhfinal = _f64(h0), _f64(dhfinal)
     pos = _i32(pos)
     Nb, Dn, L = u.shape
     N = A.shape[1]
@@ -149,15 +162,16 @@ def scan_bwd(u, delta, A, B, C, D=None, z=None, delta_bias=None, delta_softplus=
         "dD": np.empty(Dn) if D is not None else None,
         "dz": np.empty_like(u) if z is not None else None,
         "ddelta_bias": np.empty(Dn) if delta_bias is not None else None,
+        "dh0": np.empty((Nb, Dn, N)) if h0 is not None else None,
     }
     lib.pmo_scan_bwd(_ptr(u), _ptr(delta), _ptr(A), _ptr(B), _ptr(C), _ptr(D), _ptr(z),
-                     _ptr(delta_bias), int(delta_softplus), _ptr(pos), _ptr(dout),
+                     _ptr(delta_bias), int(delta_softplus), _ptr(pos), _ptr(h0), _ptr(dout), _ptr(dhfinal),
                      _ptr(g["du"]), _ptr(g["ddelta"]), _ptr(g["dA"]), _ptr(g["dB"]), _ptr(g["dC"]),
-                     _ptr(g["dD"]), _ptr(g["dz"]), _ptr(g["ddelta_bias"]), Nb, Dn, L, N)
+                     _ptr(g["dD"]), _ptr(g["dz"]), _ptr(g["ddelta_bias"]), _ptr(g["dh0"]), Nb, Dn, L, N)
     return g
 
 
-def check_positions(pos, lib=None) -> int:
+def check_positions(pos, lib=None, continued=False) -> int:
     lib = lib or load()
     pos = _i32(pos)
-    return int(lib.pmo_check_positions(_ptr(pos), pos.shape[0], pos.shape[1]))
+    return int(lib.pmo_check_positions(_ptr(pos), pos.shape[0], pos.shape[1], int(continued)))

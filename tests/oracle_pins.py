@@ -13,6 +13,11 @@ deliberately broken builds of the oracle) and raises AssertionError on failure.
   pin_library_conv    torch's conv1d (fp64, CPU) run per sequence
   pin_states          chunk-end hidden states against the geometric sum
   pin_check_positions the index contract of §3.1
+  pin_split_*         a row cut in two, the parts passing states (§5): equal to the
+                      uncut row, forward and backward (gradients chained through
+                      the passed states)
+  pin_fd_*_states     finite differences of the initial-state gradients, on rows
+                      that continue a sequence
 """
 from __future__ import annotations
 
@@ -317,9 +322,120 @@ def pin_check_positions(lib):
     assert O.check_positions(bad, lib=lib) == 3
 
 
+# ---------------------------------------------------------------------------
+# state passing across rows (§5): cutting a row and passing the states must not
+# change anything
+# ---------------------------------------------------------------------------
+
+SPLIT_ROWS = [[6, 1, 9, 2, 14], [32]]
+# cut points: inside a sequence, on a sequence start, just before a start, a part
+# shorter than the conv halo, inside the single long sequence
+SPLIT_CUTS = [(0, 3), (0, 6), (0, 15), (0, 30), (1, 1), (1, 17)]
+
+
+def _cut(p, b, c, keys):
+    first = {k: p[k][b:b + 1, ..., :c] for k in keys}
+    second = {k: p[k][b:b + 1, ..., c:] for k in keys}
+    return first, second
+
+
+def pin_split_scan(lib):
+    p = _problem(SPLIT_ROWS, Dn=2, N=3, seed=20)
+    full_out = O.scan_fwd(**_scan_args(p), lib=lib)
+    full_g = O.scan_bwd(**_scan_args(p), dout=p["dout"], lib=lib)
+    keys = ("u", "delta", "z", "B", "C", "dout", "pos")
+    for b, c in SPLIT_CUTS:
+        one, two = _cut(p, b, c, keys)
+        q1, q2 = dict(p, **one), dict(p, **two)
+        o1, h1 = O.scan_fwd(**_scan_args(q1), lib=lib, return_final=True)
+        o2, h2 = O.scan_fwd(**_scan_args(q2), lib=lib, h0=h1, return_final=True)
+        _close(np.concatenate([o1, o2], axis=-1), full_out[b:b + 1], 1e-12, f"split scan out {b},{c}")
+        _, hfull = O.scan_fwd(**_scan_args(dict(p, **{k: p[k][b:b + 1] for k in keys})), lib=lib,
+                              return_final=True)
+        _close(h2, hfull, 1e-12, f"split scan final state {b},{c}")
+        g2 = O.scan_bwd(**_scan_args(q2), dout=q2["dout"], lib=lib, h0=h1)
+        g1 = O.scan_bwd(**_scan_args(q1), dout=q1["dout"], lib=lib, dhfinal=g2["dh0"])
+        for k in ("du", "ddelta", "dz", "dB", "dC"):
+            _close(np.concatenate([g1[k], g2[k]], axis=-1), full_g[k][b:b + 1], 1e-11,
+                   f"split scan {k} {b},{c}")
+        one_row = dict(p, **{k: p[k][b:b + 1] for k in keys})
+        gr = O.scan_bwd(**_scan_args(one_row), dout=one_row["dout"], lib=lib)
+        for k in ("dA", "dD", "ddelta_bias"):
+            _close(g1[k] + g2[k], gr[k], 1e-11, f"split scan {k} {b},{c}")
+        if p["pos"][b, c] == 0:
+            assert np.all(g2["dh0"] == 0.0), "a start at the cut must stop the state's gradient"
+
+
+def pin_split_conv(lib):
+    p = _problem(SPLIT_ROWS, Dn=2, seed=21)
+    for silu in (True, False):
+        full = O.conv1d_fwd(p["x"], p["w"], p["bias"], p["pos"], silu, lib=lib)
+        for b, c in SPLIT_CUTS:
+            one, two = _cut(p, b, c, ("x", "dout", "pos"))
+            o1, f1 = O.conv1d_fwd(one["x"], p["w"], p["bias"], one["pos"], silu, lib=lib, return_final=True)
+            o2 = O.conv1d_fwd(two["x"], p["w"], p["bias"], two["pos"], silu, lib=lib, xinit=f1)
+            _close(np.concatenate([o1, o2], axis=-1), full[b:b + 1], 1e-13, f"split conv out {b},{c}")
+            gfull = O.conv1d_bwd(p["x"][b:b + 1], p["w"], p["bias"], p["pos"][b:b + 1],
+                                 p["dout"][b:b + 1], silu, lib=lib)
+            g2 = O.conv1d_bwd(two["x"], p["w"], p["bias"], two["pos"], two["dout"], silu, lib=lib, xinit=f1)
+            g1 = O.conv1d_bwd(one["x"], p["w"], p["bias"], one["pos"], one["dout"], silu, lib=lib,
+                              dxfinal=g2["dxinit"])
+            _close(np.concatenate([g1["dx"], g2["dx"]], axis=-1), gfull["dx"], 1e-12, f"split conv dx {b},{c}")
+            _close(g1["dw"] + g2["dw"], gfull["dw"], 1e-12, f"split conv dw {b},{c}")
+            _close(g1["dbias"] + g2["dbias"], gfull["dbias"], 1e-12, f"split conv dbias {b},{c}")
+
+
+def pin_fd_scan_states(lib):
+    """A row continuing a sequence (first index 5) from an initial state, with a final-state
+    gradient: finite differences of every input, the initial state included."""
+    p = _problem([[3, 9]], Dn=2, N=3, seed=22)
+    p["pos"][0, :3] = np.arange(5, 8)
+    rng = np.random.default_rng(23)
+    p["h0"] = rng.standard_normal((1, 2, 3))
+    ghf = rng.standard_normal((1, 2, 3))
+
+    def loss():
+        out, hf = O.scan_fwd(**_scan_args(p), lib=lib, h0=p["h0"], return_final=True)
+        return float(np.sum(p["dout"] * out) + np.sum(ghf * hf))
+
+    g = O.scan_bwd(**_scan_args(p), dout=p["dout"], lib=lib, h0=p["h0"], dhfinal=ghf)
+    grads = {"u": g["du"], "delta": g["ddelta"], "A": g["dA"], "B": g["dB"], "C": g["dC"],
+             "D": g["dD"], "z": g["dz"], "delta_bias": g["ddelta_bias"], "h0": g["dh0"]}
+    _fd(loss, p, list(grads), grads, "scan with states")
+
+
+def pin_fd_conv_states(lib):
+    for silu in (True, False):
+        p = _problem([[2, 1, 6]], Dn=2, seed=24 + silu)
+        p["pos"][0, :2] = np.arange(1, 3)          # continues a sequence: one tap reaches back
+        rng = np.random.default_rng(26)
+        p["xinit"] = rng.standard_normal((1, 2, 3))
+        gxf = rng.standard_normal((1, 2, 3))
+
+        def loss():
+            out, xf = O.conv1d_fwd(p["x"], p["w"], p["bias"], p["pos"], silu, lib=lib, xinit=p["xinit"],
+                                   return_final=True)
+            return float(np.sum(p["dout"] * out) + np.sum(gxf * xf))
+
+        g = O.conv1d_bwd(p["x"], p["w"], p["bias"], p["pos"], p["dout"], silu, lib=lib,
+                         xinit=p["xinit"], dxfinal=gxf)
+        grads = {"x": g["dx"], "w": g["dw"], "bias": g["dbias"], "xinit": g["dxinit"]}
+        _fd(loss, p, list(grads), grads, f"conv with states silu={silu}")
+
+
+def pin_check_positions_continued(lib):
+    pos = W.positions_from_lengths([[3, 5]], 8)
+    pos[0, :3] = [4, 5, 6]
+    assert O.check_positions(pos, lib=lib) == 0
+    assert O.check_positions(pos, lib=lib, continued=True) == -1
+    pos[0, 0] = -1
+    assert O.check_positions(pos, lib=lib, continued=True) == 0
+
+
 # cheapest first (the mutant test stops at the first pin that rejects a mutant)
 ALL_PINS = [
     pin_check_positions, pin_len1_conv, pin_len1_scan, pin_cumsum, pin_closed_conv,
     pin_closed_scan, pin_states, pin_library_conv, pin_pui_conv, pin_pui_scan, pin_fd_conv,
-    pin_fd_scan_plain, pin_fd_scan,
+    pin_fd_scan_plain, pin_fd_scan, pin_check_positions_continued, pin_split_conv, pin_split_scan,
+    pin_fd_conv_states, pin_fd_scan_states,
 ]
