@@ -123,25 +123,25 @@ class Chain:
 
         def conv_fwd():
             _lib.check("conv_fwd", lib.packmamba_causal_conv1d_fwd(
-                P(t["x"]), P(t["w"]), P(t["bias"]), P(t["pos"]), P(self.u), Nb, Dn, L, W, c, 1, sp))
+                P(t["x"]), P(t["w"]), P(t["bias"]), P(t["pos"]), None, P(self.u), None, Nb, Dn, L, W, c, 1, sp))
 
         def scan_fwd():
             _lib.check("scan_fwd", lib.packmamba_selective_scan_fwd(
                 P(self.u), P(t["delta"]), P(t["A"]), P(t["B"]), P(t["C"]), P(t["D"]), P(t["z"]),
-                P(t["delta_bias"]), 1, P(t["pos"]), P(self.out), P(self.states),
+                P(t["delta_bias"]), 1, P(t["pos"]), None, P(self.out), None, P(self.states),
                 P(self.ws_fwd), self.ws_fwd.numel(), Nb, Dn, L, N, c, sp))
 
         def scan_bwd():
             _lib.check("scan_bwd", lib.packmamba_selective_scan_bwd(
                 P(self.u), P(t["delta"]), P(t["A"]), P(t["B"]), P(t["C"]), P(t["D"]), P(t["z"]),
-                P(t["delta_bias"]), 1, P(t["pos"]), P(t["dout"]), P(self.states),
+                P(t["delta_bias"]), 1, P(t["pos"]), None, P(t["dout"]), None, P(self.states),
                 P(self.du), P(self.ddl), P(self.dA), P(self.dB), P(self.dC), P(self.dD), P(self.dz),
-                P(self.ddb), P(self.ws_scan), self.ws_scan.numel(), Nb, Dn, L, N, c, sp))
+                P(self.ddb), None, P(self.ws_scan), self.ws_scan.numel(), Nb, Dn, L, N, c, sp))
 
         def conv_bwd():
             _lib.check("conv_bwd", lib.packmamba_causal_conv1d_bwd(
-                P(t["x"]), P(t["w"]), P(t["bias"]), P(t["pos"]), P(self.du), P(self.dx), P(self.dw),
-                P(self.dcb), P(self.ws_conv), self.ws_conv.numel(), Nb, Dn, L, W, c, 1, sp))
+                P(t["x"]), P(t["w"]), P(t["bias"]), P(t["pos"]), None, P(self.du), None, P(self.dx), P(self.dw),
+                P(self.dcb), None, P(self.ws_conv), self.ws_conv.numel(), Nb, Dn, L, W, c, 1, sp))
 
         return [("conv_fwd", conv_fwd), ("scan_fwd", scan_fwd), ("scan_bwd", scan_bwd),
                 ("conv_bwd", conv_bwd)]

@@ -34,6 +34,15 @@
  *  - Precondition (not checked on the hot path): position_indices[b,0] == 0 and
  *    position_indices[b,l] is 0 or position_indices[b,l-1]+1.
  *    packmamba_check_position_indices() verifies it on demand.
+ *  - State passing across rows (the future work of §5: a long sequence cut at a
+ *    row end continues in another row).  Every operator takes optional per-row
+ *    initial states and returns final states, with their gradients.  A row that
+ *    continues a sequence has its first position index equal to that token's
+ *    position in the sequence (then any value >= 0); a 0 there starts a new
+ *    sequence and cuts the initial state off, as any start does.  Passing a
+ *    row's final states as the next part's initial states makes the two parts
+ *    compute exactly what the uncut row computes; without initial states a
+ *    continued sequence sees zeros.  All state pointers may be NULL.
  */
 #ifndef PACKMAMBA_H
 #define PACKMAMBA_H
@@ -45,7 +54,7 @@
 extern "C" {
 #endif
 
-#define PACKMAMBA_ABI_VERSION 2
+#define PACKMAMBA_ABI_VERSION 3
 
 /* dtype codes of the activation tensors */
 #define PACKMAMBA_F32 0            /* fp32 inputs, fp32 outputs */
@@ -77,12 +86,18 @@ const char* packmamba_status_string(int status);
  *   pre[b,d,l] = bias[d] + sum_{k=0}^{width-1} [k <= pos[b,l]] * weight[d,width-1-k] * x[b,d,l-k]
  *   out = silu ? pre * sigmoid(pre) : pre
  * The tap that reaches k tokens back is used only if it stays inside the output
- * token's own sequence; weight[d, width-1] multiplies the current token.
+ * token's own sequence; weight[d, width-1] multiplies the current token.  A tap
+ * reaching before the row (a continued sequence) reads initial_x.
  *   x, out: dtype (batch, dim, seqlen); weight (dim, width); bias (dim) or NULL;
  *   width in [2, 4].
+ *   initial_x: NULL, or (batch, dim, width-1) in x's storage type: the inputs of
+ *   the width-1 tokens before each row, token -1 last (NULL reads zeros).
+ *   final_x: NULL, or (batch, dim, width-1) in x's storage type, receives each
+ *   row's last width-1 inputs, copied (from initial_x where the row is shorter).
  */
 int packmamba_causal_conv1d_fwd(const void* x, const float* weight, const float* bias,
-                                const int32_t* position_indices, void* out,
+                                const int32_t* position_indices, const void* initial_x,
+                                void* out, void* final_x,
                                 int64_t batch, int64_t dim, int64_t seqlen, int32_t width,
                                 int32_t dtype, int32_t silu, void* stream);
 
@@ -98,10 +113,15 @@ size_t packmamba_causal_conv1d_bwd_workspace_size(int64_t batch, int64_t dim, in
  *   dbias[d] = sum_{b,l} g[b,d,l].
  *   dx: dtype; dweight (dim, width) and dbias (dim) are overwritten; dbias must
  *   be NULL iff bias is NULL.  The parameter sums are deterministic (fixed order).
+ *   initial_x: as in the forward.  dfinal_x: NULL (zero), or the gradient of
+ *   final_x, (batch, dim, width-1) in dout's storage type.  dinitial_x: the
+ *   gradient of initial_x, (batch, dim, width-1) in dx's type; it must be NULL iff
+ *   initial_x is NULL.
  */
 int packmamba_causal_conv1d_bwd(const void* x, const float* weight, const float* bias,
-                                const int32_t* position_indices, const void* dout,
-                                void* dx, float* dweight, float* dbias,
+                                const int32_t* position_indices, const void* initial_x,
+                                const void* dout, const void* dfinal_x,
+                                void* dx, float* dweight, float* dbias, void* dinitial_x,
                                 void* workspace, size_t workspace_bytes,
                                 int64_t batch, int64_t dim, int64_t seqlen, int32_t width,
                                 int32_t dtype, int32_t silu, void* stream);
@@ -132,7 +152,9 @@ size_t packmamba_selective_scan_fwd_workspace_size(int64_t batch, int64_t dim, i
  *   packmamba_selective_scan_fwd_saved_states_size() bytes that receives h after
  *   token min((c+1)*PACKMAMBA_STATE_STRIDE, seqlen)-1 for every chunk c, laid out
  *   (batch, dim, chunk, dstate); the backward reuses it instead of recomputing.
- *   `out` may be NULL when saved_states is not (states only).
+ *   `out` may be NULL when saved_states or final_state is not (states only).
+ *   initial_state: NULL (zeros), or (batch, dim, dstate) float: h before each row.
+ *   final_state: NULL, or (batch, dim, dstate) float, receives h after each row.
  *   workspace: device scratch of packmamba_selective_scan_fwd_workspace_size()
  *   bytes, owned by the caller and not read after the call's kernels finish; may
  *   be NULL when that size is 0.  Too small or missing: PACKMAMBA_ERR_WORKSPACE.
@@ -140,7 +162,8 @@ size_t packmamba_selective_scan_fwd_workspace_size(int64_t batch, int64_t dim, i
 int packmamba_selective_scan_fwd(const void* u, const void* delta, const float* A,
                                  const void* B, const void* C, const float* D, const void* z,
                                  const float* delta_bias, int32_t delta_softplus,
-                                 const int32_t* position_indices, void* out, float* saved_states,
+                                 const int32_t* position_indices, const float* initial_state,
+                                 void* out, float* final_state, float* saved_states,
                                  void* workspace, size_t workspace_bytes,
                                  int64_t batch, int64_t dim, int64_t seqlen, int32_t dstate,
                                  int32_t dtype, void* stream);
@@ -156,21 +179,25 @@ size_t packmamba_selective_scan_bwd_workspace_size(int64_t batch, int64_t dim, i
  *   dh_l = Abar_{l+1} * dh_{l+1} + C_l * dy_l,   Abar_{l+1} = 0 where token l+1 starts a sequence,
  * carries the matching reset; a reset multiplier is the constant 0, so no
  * gradient flows to delta or A through it.
- *   Inputs: as the forward, same order, plus dout (dtype) and saved_states
- *   (NULL: recomputed into the workspace).
+ *   Inputs: as the forward, same order (initial_state included), plus dout
+ *   (dtype), dfinal_state (NULL: zero; else the gradient of final_state,
+ *   (batch, dim, dstate) float, entering h after the row's last token) and
+ *   saved_states (NULL: recomputed into the workspace).
  *   Outputs (overwritten): du, ddelta (dtype, like u); dA (dim, dstate);
  *   dB, dC (batch, dstate, seqlen) float; dD (dim) iff D != NULL;
- *   dz (dtype) iff z != NULL; ddelta_bias (dim) iff delta_bias != NULL.
+ *   dz (dtype) iff z != NULL; ddelta_bias (dim) iff delta_bias != NULL;
+ *   dinitial_state (batch, dim, dstate) float iff initial_state != NULL.
  *   Sums over channels and tokens use per-block partials in the workspace and a
  *   second pass in fixed order: results are bitwise reproducible.
  */
 int packmamba_selective_scan_bwd(const void* u, const void* delta, const float* A,
                                  const void* B, const void* C, const float* D, const void* z,
                                  const float* delta_bias, int32_t delta_softplus,
-                                 const int32_t* position_indices, const void* dout,
+                                 const int32_t* position_indices, const float* initial_state,
+                                 const void* dout, const float* dfinal_state,
                                  const float* saved_states,
                                  void* du, void* ddelta, float* dA, float* dB, float* dC,
-                                 float* dD, void* dz, float* ddelta_bias,
+                                 float* dD, void* dz, float* ddelta_bias, float* dinitial_state,
                                  void* workspace, size_t workspace_bytes,
                                  int64_t batch, int64_t dim, int64_t seqlen, int32_t dstate,
                                  int32_t dtype, void* stream);
@@ -179,9 +206,11 @@ int packmamba_selective_scan_bwd(const void* u, const void* delta, const float* 
  * Checks the index contract of §3.1 on the device: stores 1 to *d_flag (a device
  * int32 the caller zeroes beforehand) if any token violates
  * "pos[b,0] == 0 and pos[b,l] in {0, pos[b,l-1]+1}"; leaves it untouched otherwise.
+ * With continued != 0, rows may continue a sequence: pos[b,0] >= 0 is accepted.
  */
 int packmamba_check_position_indices(const int32_t* position_indices, int64_t batch,
-                                     int64_t seqlen, int32_t* d_flag, void* stream);
+                                     int64_t seqlen, int32_t continued, int32_t* d_flag,
+                                     void* stream);
 
 #ifdef __cplusplus
 }

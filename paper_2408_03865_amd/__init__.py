@@ -11,6 +11,15 @@ status.  Nothing is computed here.
                                      return_states=True)
     grads = selective_scan_bwd(u, delta, A, B, C, D, z, delta_bias, True, position_indices, dout,
                                saved_states=states)
+
+A sequence cut at a row end continues in another row when the second part is given
+the first part's final states (the future work of §5):
+    out1, xf = causal_conv1d_fwd(x1, w, bias, pos1, return_final=True)
+    out2 = causal_conv1d_fwd(x2, w, bias, pos2, initial_x=xf)
+    y1, hf = selective_scan_fwd(..., pos1, return_final=True)
+    y2 = selective_scan_fwd(..., pos2, initial_state=hf)
+and in the backward the second part's initial-state gradients are the first part's
+final-state gradients (dfinal_x, dfinal_state).
 """
 from __future__ import annotations
 
@@ -58,19 +67,26 @@ def _workspace(nbytes: int, device):
     return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
 
 
-def causal_conv1d_fwd(x, weight, bias, position_indices, silu: bool = True, out_f32: bool = False):
-    """out_f32: for bf16 x, return fp32 outputs (the values before the bf16 rounding)."""
+def causal_conv1d_fwd(x, weight, bias, position_indices, silu: bool = True, out_f32: bool = False,
+                      initial_x=None, return_final: bool = False):
+    """out_f32: for bf16 x, return fp32 outputs (the values before the bf16 rounding).
+    initial_x: (batch, dim, width-1) in x's dtype; return_final adds the row's last
+    width-1 inputs to the result."""
+    torch = _torch()
     Nb, Dn, L = x.shape
+    W = weight.shape[1]
     out = _empty_out(x, out_f32)
-    st = load().packmamba_causal_conv1d_fwd(_p(x), _p(weight), _p(bias), _p(position_indices), _p(out),
-                                            Nb, Dn, L, weight.shape[1], _code(x, out_f32), int(silu),
-                                            _stream(x))
+    fin = torch.empty((Nb, Dn, W - 1), dtype=x.dtype, device=x.device) if return_final else None
+    st = load().packmamba_causal_conv1d_fwd(_p(x), _p(weight), _p(bias), _p(position_indices),
+                                            _p(initial_x), _p(out), _p(fin), Nb, Dn, L, W,
+                                            _code(x, out_f32), int(silu), _stream(x))
     _lib.check("packmamba_causal_conv1d_fwd", st)
-    return out
+    return (out, fin) if return_final else out
 
 
 def causal_conv1d_bwd(x, weight, bias, position_indices, dout, silu: bool = True, workspace=None,
-                      out_f32: bool = False):
+                      out_f32: bool = False, initial_x=None, dfinal_x=None):
+    """(dx, dweight, dbias), plus dinitial_x when initial_x is given."""
     torch = _torch()
     Nb, Dn, L = x.shape
     W = weight.shape[1]
@@ -78,13 +94,17 @@ def causal_conv1d_bwd(x, weight, bias, position_indices, dout, silu: bool = True
     dx = _empty_out(x, out_f32)
     dw = torch.empty_like(weight)
     db = torch.empty_like(bias) if bias is not None else None
+    dinit = None
+    if initial_x is not None:
+        dinit = torch.empty((Nb, Dn, W - 1), dtype=dx.dtype, device=x.device)
     need = lib.packmamba_causal_conv1d_bwd_workspace_size(Nb, Dn, L, W)
     ws = workspace if workspace is not None else _workspace(need, x.device)
-    st = lib.packmamba_causal_conv1d_bwd(_p(x), _p(weight), _p(bias), _p(position_indices), _p(dout),
-                                         _p(dx), _p(dw), _p(db), _p(ws), ws.numel(), Nb, Dn, L, W,
-                                         _code(x, out_f32), int(silu), _stream(x))
+    st = lib.packmamba_causal_conv1d_bwd(_p(x), _p(weight), _p(bias), _p(position_indices), _p(initial_x),
+                                         _p(dout), _p(dfinal_x), _p(dx), _p(dw), _p(db), _p(dinit),
+                                         _p(ws), ws.numel(), Nb, Dn, L, W, _code(x, out_f32), int(silu),
+                                         _stream(x))
     _lib.check("packmamba_causal_conv1d_bwd", st)
-    return dx, dw, db
+    return (dx, dw, db) if initial_x is None else (dx, dw, db, dinit)
 
 
 def segments(batch: int, dim: int, seqlen: int) -> int:
@@ -104,7 +124,11 @@ def saved_states_size(batch: int, dim: int, seqlen: int, dstate: int = 16) -> in
 
 
 def selective_scan_fwd(u, delta, A, B, C, D, z, delta_bias, delta_softplus, position_indices,
-                       return_states: bool = False, out=True, out_f32: bool = False, workspace=None):
+                       return_states: bool = False, out=True, out_f32: bool = False, workspace=None,
+                       initial_state=None, return_final: bool = False):
+    """out, followed by the saved states (return_states) and the final state
+    (return_final, (batch, dim, dstate) fp32) when asked for; initial_state is
+    (batch, dim, dstate) fp32."""
     torch = _torch()
     Nb, Dn, L = u.shape
     N = A.shape[1]
@@ -116,16 +140,19 @@ def selective_scan_fwd(u, delta, A, B, C, D, z, delta_bias, delta_softplus, posi
     if return_states:
         nch = (L + STATE_STRIDE - 1) // STATE_STRIDE
         states = torch.empty((Nb, Dn, nch, N), dtype=torch.float32, device=u.device)
+    fin = torch.empty((Nb, Dn, N), dtype=torch.float32, device=u.device) if return_final else None
     st = lib.packmamba_selective_scan_fwd(
         _p(u), _p(delta), _p(A), _p(B), _p(C), _p(D), _p(z), _p(delta_bias), int(delta_softplus),
-        _p(position_indices), _p(o), _p(states), _p(ws), 0 if ws is None else ws.numel(),
-        Nb, Dn, L, N, _code(u, out_f32), _stream(u))
+        _p(position_indices), _p(initial_state), _p(o), _p(fin), _p(states), _p(ws),
+        0 if ws is None else ws.numel(), Nb, Dn, L, N, _code(u, out_f32), _stream(u))
     _lib.check("packmamba_selective_scan_fwd", st)
-    return (o, states) if return_states else o
+    res = (o,) + ((states,) if return_states else ()) + ((fin,) if return_final else ())
+    return res if len(res) > 1 else o
 
 
 def selective_scan_bwd(u, delta, A, B, C, D, z, delta_bias, delta_softplus, position_indices, dout,
-                       saved_states=None, workspace=None, out_f32: bool = False) -> Dict[str, object]:
+                       saved_states=None, workspace=None, out_f32: bool = False, initial_state=None,
+                       dfinal_state=None) -> Dict[str, object]:
     torch = _torch()
     Nb, Dn, L = u.shape
     N = A.shape[1]
@@ -137,24 +164,27 @@ def selective_scan_bwd(u, delta, A, B, C, D, z, delta_bias, delta_softplus, posi
         "dD": torch.empty_like(D) if D is not None else None,
         "dz": _empty_out(z, out_f32) if z is not None else None,
         "ddelta_bias": torch.empty_like(delta_bias) if delta_bias is not None else None,
+        "dinitial_state": torch.empty_like(initial_state) if initial_state is not None else None,
     }
     need = lib.packmamba_selective_scan_bwd_workspace_size(Nb, Dn, L, N)
     ws = workspace if workspace is not None else _workspace(need, u.device)
     st = lib.packmamba_selective_scan_bwd(
         _p(u), _p(delta), _p(A), _p(B), _p(C), _p(D), _p(z), _p(delta_bias), int(delta_softplus),
-        _p(position_indices), _p(dout), _p(saved_states), _p(g["du"]), _p(g["ddelta"]), _p(g["dA"]),
-        _p(g["dB"]), _p(g["dC"]), _p(g["dD"]), _p(g["dz"]), _p(g["ddelta_bias"]), _p(ws), ws.numel(),
+        _p(position_indices), _p(initial_state), _p(dout), _p(dfinal_state), _p(saved_states),
+        _p(g["du"]), _p(g["ddelta"]), _p(g["dA"]), _p(g["dB"]), _p(g["dC"]), _p(g["dD"]), _p(g["dz"]),
+        _p(g["ddelta_bias"]), _p(g["dinitial_state"]), _p(ws), ws.numel(),
         Nb, Dn, L, N, _code(u, out_f32), _stream(u))
     _lib.check("packmamba_selective_scan_bwd", st)
     return g
 
 
-def check_position_indices(position_indices) -> bool:
-    """True if the indices satisfy the packing contract (checked on the device)."""
+def check_position_indices(position_indices, continued: bool = False) -> bool:
+    """True if the indices satisfy the packing contract (checked on the device);
+    with ``continued``, rows may start inside a sequence carried over from another row."""
     torch = _torch()
     flag = torch.zeros(4, dtype=torch.int32, device=position_indices.device)
     Nb, L = position_indices.shape
-    st = load().packmamba_check_position_indices(_p(position_indices), Nb, L, _p(flag),
+    st = load().packmamba_check_position_indices(_p(position_indices), Nb, L, int(continued), _p(flag),
                                                  _stream(position_indices))
     _lib.check("packmamba_check_position_indices", st)
     return int(flag[0].item()) == 0

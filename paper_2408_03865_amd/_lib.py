@@ -15,7 +15,7 @@ LIB_PATH = os.path.join(HERE, "libpackmamba.so")
 
 F32, BF16, BF16_F32OUT = 0, 1, 2
 STATE_STRIDE = 128
-ABI_VERSION = 2
+ABI_VERSION = 3
 
 STATUS = {0: "OK", 1: "ERR_NULL", 2: "ERR_SHAPE", 3: "ERR_UNSUPPORTED", 4: "ERR_ALIGN",
           5: "ERR_WORKSPACE", 6: "ERR_LAUNCH"}
@@ -52,19 +52,19 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.packmamba_abi_version.restype = ctypes.c_int
     lib.packmamba_status_string.argtypes = [ctypes.c_int]
     lib.packmamba_status_string.restype = ctypes.c_char_p
-    lib.packmamba_causal_conv1d_fwd.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, i32, i32, i32, vp]
+    lib.packmamba_causal_conv1d_fwd.argtypes = [vp] * 7 + [i64, i64, i64, i32, i32, i32, vp]
     lib.packmamba_causal_conv1d_bwd_workspace_size.argtypes = [i64, i64, i64, i32]
     lib.packmamba_causal_conv1d_bwd_workspace_size.restype = sz
-    lib.packmamba_causal_conv1d_bwd.argtypes = [vp] * 9 + [sz, i64, i64, i64, i32, i32, i32, vp]
+    lib.packmamba_causal_conv1d_bwd.argtypes = [vp] * 12 + [sz, i64, i64, i64, i32, i32, i32, vp]
     lib.packmamba_selective_scan_fwd_saved_states_size.argtypes = [i64, i64, i64, i32]
     lib.packmamba_selective_scan_fwd_saved_states_size.restype = sz
     lib.packmamba_selective_scan_fwd_workspace_size.argtypes = [i64, i64, i64, i32]
     lib.packmamba_selective_scan_fwd_workspace_size.restype = sz
-    lib.packmamba_selective_scan_fwd.argtypes = [vp] * 8 + [i32, vp, vp, vp, vp, sz, i64, i64, i64, i32, i32, vp]
+    lib.packmamba_selective_scan_fwd.argtypes = [vp] * 8 + [i32] + [vp] * 6 + [sz, i64, i64, i64, i32, i32, vp]
     lib.packmamba_selective_scan_bwd_workspace_size.argtypes = [i64, i64, i64, i32]
     lib.packmamba_selective_scan_bwd_workspace_size.restype = sz
-    lib.packmamba_selective_scan_bwd.argtypes = ([vp] * 8 + [i32] + [vp] * 12 + [sz, i64, i64, i64, i32, i32, vp])
-    lib.packmamba_check_position_indices.argtypes = [vp, i64, i64, vp, vp]
+    lib.packmamba_selective_scan_bwd.argtypes = ([vp] * 8 + [i32] + [vp] * 15 + [sz, i64, i64, i64, i32, i32, vp])
+    lib.packmamba_check_position_indices.argtypes = [vp, i64, i64, i32, vp, vp]
     for name in ("packmamba_causal_conv1d_fwd", "packmamba_causal_conv1d_bwd",
                  "packmamba_selective_scan_fwd", "packmamba_selective_scan_bwd",
                  "packmamba_check_position_indices"):

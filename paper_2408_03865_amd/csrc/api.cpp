@@ -100,18 +100,20 @@ const char* packmamba_status_string(int status) {
 }
 
 int packmamba_causal_conv1d_fwd(const void* x, const float* weight, const float* bias,
-                                const int32_t* position_indices, void* out, int64_t batch,
-                                int64_t dim, int64_t seqlen, int32_t width, int32_t dtype,
-                                int32_t silu, void* stream) {
+                                const int32_t* position_indices, const void* initial_x,
+                                void* out, void* final_x, int64_t batch, int64_t dim,
+                                int64_t seqlen, int32_t width, int32_t dtype, int32_t silu,
+                                void* stream) {
     if (!x || !weight || !position_indices || !out) return PACKMAMBA_ERR_NULL;
     if (int e = check_shape(batch, dim, seqlen)) return e;
     if (int e = check_dtype(dtype)) return e;
     if (width < 2 || width > 4) return PACKMAMBA_ERR_UNSUPPORTED;
     if (!aligned16(x) || !aligned16(weight) || !aligned16(bias) || !aligned16(position_indices) ||
-        !aligned16(out))
+        !aligned16(out) || !aligned16(initial_x) || !aligned16(final_x))
         return PACKMAMBA_ERR_ALIGN;
     pm::ConvArgs a{};
     a.x = x; a.w = weight; a.bias = bias; a.pos = position_indices; a.out = out;
+    a.xinit = initial_x; a.xfinal = final_x;
     a.batch = batch; a.dim = dim; a.seqlen = seqlen; a.width = width; a.dtype = dtype;
     a.silu = silu ? 1 : 0;
     return launch_status(pm::launch_conv1d_fwd(a, (hipStream_t)stream));
@@ -124,24 +126,28 @@ size_t packmamba_causal_conv1d_bwd_workspace_size(int64_t batch, int64_t dim, in
 }
 
 int packmamba_causal_conv1d_bwd(const void* x, const float* weight, const float* bias,
-                                const int32_t* position_indices, const void* dout, void* dx,
-                                float* dweight, float* dbias, void* workspace,
+                                const int32_t* position_indices, const void* initial_x,
+                                const void* dout, const void* dfinal_x, void* dx, float* dweight,
+                                float* dbias, void* dinitial_x, void* workspace,
                                 size_t workspace_bytes, int64_t batch, int64_t dim, int64_t seqlen,
                                 int32_t width, int32_t dtype, int32_t silu, void* stream) {
     if (!x || !weight || !position_indices || !dout || !dx || !dweight) return PACKMAMBA_ERR_NULL;
     if ((bias == nullptr) != (dbias == nullptr)) return PACKMAMBA_ERR_NULL;
+    if ((initial_x == nullptr) != (dinitial_x == nullptr)) return PACKMAMBA_ERR_NULL;
     if (int e = check_shape(batch, dim, seqlen)) return e;
     if (int e = check_dtype(dtype)) return e;
     if (width < 2 || width > 4) return PACKMAMBA_ERR_UNSUPPORTED;
     if (!aligned16(x) || !aligned16(weight) || !aligned16(bias) || !aligned16(position_indices) ||
         !aligned16(dout) || !aligned16(dx) || !aligned16(dweight) || !aligned16(dbias) ||
-        !aligned16(workspace))
+        !aligned16(workspace) || !aligned16(initial_x) || !aligned16(dfinal_x) ||
+        !aligned16(dinitial_x))
         return PACKMAMBA_ERR_ALIGN;
     const size_t need = packmamba_causal_conv1d_bwd_workspace_size(batch, dim, seqlen, width);
     if (!workspace || workspace_bytes < need) return PACKMAMBA_ERR_WORKSPACE;
     pm::ConvArgs a{};
     a.x = x; a.w = weight; a.bias = bias; a.pos = position_indices; a.dout = dout; a.out = dx;
     a.dw = dweight; a.dbias = dbias; a.partial = static_cast<float*>(workspace);
+    a.xinit = initial_x; a.dxfinal = dfinal_x; a.dxinit = dinitial_x;
     a.batch = batch; a.dim = dim; a.seqlen = seqlen; a.width = width; a.dtype = dtype;
     a.silu = silu ? 1 : 0;
     return launch_status(pm::launch_conv1d_bwd(a, (hipStream_t)stream));
@@ -162,19 +168,20 @@ size_t packmamba_selective_scan_fwd_workspace_size(int64_t batch, int64_t dim, i
 int packmamba_selective_scan_fwd(const void* u, const void* delta, const float* A, const void* B,
                                  const void* C, const float* D, const void* z,
                                  const float* delta_bias, int32_t delta_softplus,
-                                 const int32_t* position_indices, void* out, float* saved_states,
+                                 const int32_t* position_indices, const float* initial_state,
+                                 void* out, float* final_state, float* saved_states,
                                  void* workspace, size_t workspace_bytes, int64_t batch,
                                  int64_t dim, int64_t seqlen, int32_t dstate, int32_t dtype,
                                  void* stream) {
     if (!u || !delta || !A || !B || !C || !position_indices) return PACKMAMBA_ERR_NULL;
-    if (!out && !saved_states) return PACKMAMBA_ERR_NULL;
+    if (!out && !saved_states && !final_state) return PACKMAMBA_ERR_NULL;
     if (int e = check_shape(batch, dim, seqlen)) return e;
     if (int e = check_dtype(dtype)) return e;
     if (dstate != kN) return PACKMAMBA_ERR_UNSUPPORTED;
     if (!aligned16(u) || !aligned16(delta) || !aligned16(A) || !aligned16(B) || !aligned16(C) ||
         !aligned16(D) || !aligned16(z) || !aligned16(delta_bias) ||
         !aligned16(position_indices) || !aligned16(out) || !aligned16(saved_states) ||
-        !aligned16(workspace))
+        !aligned16(workspace) || !aligned16(initial_state) || !aligned16(final_state))
         return PACKMAMBA_ERR_ALIGN;
     const SegWs w = seg_ws(batch, dim, seqlen);
     if (w.total && (!workspace || workspace_bytes < w.total)) return PACKMAMBA_ERR_WORKSPACE;
@@ -182,7 +189,7 @@ int packmamba_selective_scan_fwd(const void* u, const void* delta, const float* 
     set_seg_ws(a, static_cast<char*>(workspace), w);
     a.u = u; a.delta = delta; a.A = A; a.B = B; a.C = C; a.D = D; a.z = z;
     a.delta_bias = delta_bias; a.pos = position_indices; a.softplus = delta_softplus ? 1 : 0;
-    a.out = out; a.states = saved_states;
+    a.out = out; a.states = saved_states; a.h0 = initial_state; a.hfinal = final_state;
     a.batch = batch; a.dim = dim; a.seqlen = seqlen; a.dstate = dstate; a.dtype = dtype;
     return launch_status(pm::launch_scan_fwd(a, (hipStream_t)stream));
 }
@@ -196,22 +203,26 @@ size_t packmamba_selective_scan_bwd_workspace_size(int64_t batch, int64_t dim, i
 int packmamba_selective_scan_bwd(const void* u, const void* delta, const float* A, const void* B,
                                  const void* C, const float* D, const void* z,
                                  const float* delta_bias, int32_t delta_softplus,
-                                 const int32_t* position_indices, const void* dout,
+                                 const int32_t* position_indices, const float* initial_state,
+                                 const void* dout, const float* dfinal_state,
                                  const float* saved_states, void* du, void* ddelta, float* dA,
                                  float* dB, float* dC, float* dD, void* dz, float* ddelta_bias,
+                                 float* dinitial_state,
                                  void* workspace, size_t workspace_bytes, int64_t batch,
                                  int64_t dim, int64_t seqlen, int32_t dstate, int32_t dtype,
                                  void* stream) {
     if (!u || !delta || !A || !B || !C || !position_indices || !dout) return PACKMAMBA_ERR_NULL;
     if (!du || !ddelta || !dA || !dB || !dC) return PACKMAMBA_ERR_NULL;
     if ((D == nullptr) != (dD == nullptr) || (z == nullptr) != (dz == nullptr) ||
-        (delta_bias == nullptr) != (ddelta_bias == nullptr))
+        (delta_bias == nullptr) != (ddelta_bias == nullptr) ||
+        (initial_state == nullptr) != (dinitial_state == nullptr))
         return PACKMAMBA_ERR_NULL;
     if (int e = check_shape(batch, dim, seqlen)) return e;
     if (int e = check_dtype(dtype)) return e;
     if (dstate != kN) return PACKMAMBA_ERR_UNSUPPORTED;
     const void* ptrs[] = {u, delta, A, B, C, D, z, delta_bias, position_indices, dout,
-                          saved_states, du, ddelta, dA, dB, dC, dD, dz, ddelta_bias, workspace};
+                          saved_states, du, ddelta, dA, dB, dC, dD, dz, ddelta_bias, workspace,
+                          initial_state, dfinal_state, dinitial_state};
     for (const void* p : ptrs)
         if (!aligned16(p)) return PACKMAMBA_ERR_ALIGN;
     const ScanWs w = scan_ws(batch, dim, seqlen);
@@ -221,6 +232,7 @@ int packmamba_selective_scan_bwd(const void* u, const void* delta, const float* 
     a.u = u; a.delta = delta; a.A = A; a.B = B; a.C = C; a.D = D; a.z = z;
     a.delta_bias = delta_bias; a.pos = position_indices; a.softplus = delta_softplus ? 1 : 0;
     a.batch = batch; a.dim = dim; a.seqlen = seqlen; a.dstate = dstate; a.dtype = dtype;
+    a.h0 = initial_state;
     hipStream_t s = (hipStream_t)stream;
     // the forward recompute below and the backward run one after the other on the
     // stream, so they share the segment workspace
@@ -234,19 +246,20 @@ int packmamba_selective_scan_bwd(const void* u, const void* delta, const float* 
         if (int e = launch_status(pm::launch_scan_fwd(a, s))) return e;
     }
     a.dout = dout; a.du = du; a.ddelta = ddelta; a.dz = dz; a.dA = dA; a.dB = dB; a.dC = dC;
-    a.dD = dD; a.ddelta_bias = ddelta_bias;
+    a.dD = dD; a.ddelta_bias = ddelta_bias; a.dhfinal = dfinal_state; a.dh0 = dinitial_state;
     a.part_bc = reinterpret_cast<float*>(ws);
     a.part_chan = reinterpret_cast<float*>(ws + w.part_bc);
     return launch_status(pm::launch_scan_bwd(a, s));
 }
 
 int packmamba_check_position_indices(const int32_t* position_indices, int64_t batch,
-                                     int64_t seqlen, int32_t* d_flag, void* stream) {
+                                     int64_t seqlen, int32_t continued, int32_t* d_flag,
+                                     void* stream) {
     if (!position_indices || !d_flag) return PACKMAMBA_ERR_NULL;
     if (batch <= 0 || seqlen <= 0 || batch > kMaxElems / seqlen) return PACKMAMBA_ERR_SHAPE;
     if (!aligned16(position_indices)) return PACKMAMBA_ERR_ALIGN;
-    return launch_status(pm::launch_check_pos(position_indices, batch, seqlen, d_flag,
-                                              (hipStream_t)stream));
+    return launch_status(pm::launch_check_pos(position_indices, batch, seqlen, continued ? 1 : 0,
+                                              d_flag, (hipStream_t)stream));
 }
 
 }  // extern "C"

@@ -35,6 +35,28 @@ __device__ __forceinline__ void load_pos(const int32_t* __restrict__ pr, int64_t
     }
 }
 
+// Per-row states of a sequence cut at a row end (§5): (batch*dim, W-1) arrays, or
+// null.  xinit holds the W-1 inputs before the row (token -1 last), xfinal the
+// row's last W-1 inputs; dxfinal and dxinit are their gradients.
+template <typename T, typename TO>
+struct ConvStates {
+    const T* xinit;
+    T* xfinal;
+    const T* dxfinal;
+    TO* dxinit;
+};
+
+// The W-1 tokens before the row into xs[kTok-W+1 .. kTok-1] (zeros without xinit).
+template <typename T, int W>
+__device__ __forceinline__ void load_row_halo(const T* __restrict__ xinit, int64_t row, float* xs) {
+#pragma unroll
+    for (int i = 0; i < kTok; ++i) xs[i] = 0.0f;
+    if (xinit) {
+#pragma unroll
+        for (int t = 0; t < W - 1; ++t) xs[kTok - (W - 1) + t] = Storage<T>::load1(xinit + row * (W - 1) + t);
+    }
+}
+
 // pre-activation of the token at index i of `xs`, where xs[kTok + t] holds token
 // l0 + t and xs[kTok - 1 - t] holds token l0 - 1 - t
 template <int W>
@@ -49,8 +71,8 @@ __device__ __forceinline__ float conv_pre(const float* xs, int i, int p, const f
 template <typename T, typename TO, int W>
 __global__ __launch_bounds__(kThreads) void conv1d_fwd_kernel(
     const T* __restrict__ x, const float* __restrict__ w, const float* __restrict__ bias,
-    const int32_t* __restrict__ pos, TO* __restrict__ out, int64_t dim, int64_t L, int silu,
-    int vec, int pvec) {
+    const int32_t* __restrict__ pos, TO* __restrict__ out, ConvStates<T, TO> st, int64_t dim,
+    int64_t L, int silu, int vec, int pvec) {
     const int64_t row = blockIdx.x;
     const int64_t b = row / dim, d = row - b * dim;
     const T* xr = x + row * L;
@@ -65,10 +87,7 @@ __global__ __launch_bounds__(kThreads) void conv1d_fwd_kernel(
         float xs[2 * kTok];
         load_run<T, kTok>(xr, l0, L, vec, xs + kTok);
         if (l0 > 0) load_run<T, kTok>(xr, l0 - kTok, L, vec, xs);
-        else {
-#pragma unroll
-            for (int i = 0; i < kTok; ++i) xs[i] = 0.0f;
-        }
+        else load_row_halo<T, W>(st.xinit, row, xs);
         int p[kTok];
         load_pos(pr, l0, L, pvec, p);
         float o[kTok];
@@ -78,6 +97,17 @@ __global__ __launch_bounds__(kThreads) void conv1d_fwd_kernel(
             o[i] = silu ? v * sigmoid_f(v) : v;
         }
         store_run<TO, kTok>(orow, l0, L, vec, o);
+    }
+    // the row's last W-1 inputs, copied as stored (reaching into xinit for short rows)
+    if (st.xfinal && threadIdx.x == 0) {
+#pragma unroll
+        for (int i = 0; i < W - 1; ++i) {
+            const int64_t m = L - (W - 1) + i;
+            T v{};
+            if (m >= 0) v = xr[m];
+            else if (st.xinit) v = st.xinit[row * (W - 1) + (W - 1) + m];
+            st.xfinal[row * (W - 1) + i] = v;
+        }
     }
 }
 
@@ -106,12 +136,15 @@ __device__ __forceinline__ void block_sum(float* v, float* lds /* NV * (kThreads
 }
 
 // Backward: each thread owns KT consecutive tokens per step and also recomputes
-// the activation gradient of the next W-1 tokens (the reverse-index halo).
-template <typename T, typename TO, int W, int KT>
+// the activation gradient of the next W-1 tokens (the reverse-index halo).  DXF:
+// a final-input gradient is given (a separate instantiation, so that the common
+// path keeps its register count).
+template <typename T, typename TO, int W, int KT, bool DXF>
 __global__ __launch_bounds__(kThreads) void conv1d_bwd_kernel(
     const T* __restrict__ x, const float* __restrict__ w, const float* __restrict__ bias,
     const int32_t* __restrict__ pos, const T* __restrict__ dout, TO* __restrict__ dx,
-    float* __restrict__ partial, int64_t dim, int64_t L, int silu, int vec, int pvec) {
+    float* __restrict__ partial, ConvStates<T, TO> st, int64_t dim, int64_t L, int silu, int vec,
+    int pvec) {
     __shared__ float red[(W + 1) * (kThreads / 64)];
     const int64_t row = blockIdx.x;
     const int64_t b = row / dim, d = row - b * dim;
@@ -131,10 +164,7 @@ __global__ __launch_bounds__(kThreads) void conv1d_bwd_kernel(
         // x for tokens l0-8 .. l0+KT+7 (pre-activations of this run and the next W-1 tokens)
         float xs[kTok + KT + kTok];
         if (l0 > 0) load_run<T, kTok>(xr, l0 - kTok, L, vec, xs);
-        else {
-#pragma unroll
-            for (int i = 0; i < kTok; ++i) xs[i] = 0.0f;
-        }
+        else load_row_halo<T, W>(st.xinit, row, xs);
         load_run<T, KT>(xr, l0, L, vec, xs + kTok);
         load_run<T, kTok>(xr, l0 + KT, L, vec, xs + kTok + KT);
         float gs[KT + kTok];
@@ -167,6 +197,14 @@ __global__ __launch_bounds__(kThreads) void conv1d_bwd_kernel(
             for (int k = 1; k < W; ++k) a = fmaf(wk[W - 1 - k], gm[k][i + k], a);
             o[i] = a;
         }
+        // the final inputs are copies of the last W-1 inputs: their gradient adds in
+        if (DXF && l0 + KT > L - (W - 1)) {
+#pragma unroll
+            for (int i = 0; i < KT; ++i) {
+                const int64_t j = l0 + i - (L - (W - 1));
+                if (j >= 0 && l0 + i < L) o[i] += Storage<T>::load1(st.dxfinal + row * (W - 1) + j);
+            }
+        }
         store_run<TO, KT>(dxr, l0, L, vec, o);
         // parameter gradients from this thread's own tokens
 #pragma unroll
@@ -174,6 +212,37 @@ __global__ __launch_bounds__(kThreads) void conv1d_bwd_kernel(
 #pragma unroll
             for (int k = 0; k < W; ++k) acc[W - 1 - k] = fmaf(gm[k][i], xs[kTok + i - k], acc[W - 1 - k]);
             acc[W] += gm[0][i];
+        }
+    }
+    // gradient of the inputs before the row, by one thread: initial input j (token
+    // j-W+1) meets output token t <= j through tap k = t-j+W-1 (weight w[j-t]), live
+    // iff k <= pos[t]; the activation gradient of those W-1 tokens is recomputed
+    if (st.dxinit && threadIdx.x == 0) {
+        float xs[2 * kTok], gs[kTok];
+        int p[kTok];
+        load_row_halo<T, W>(st.xinit, row, xs);
+        load_run<T, kTok>(xr, 0, L, vec, xs + kTok);
+        load_run<T, kTok>(gr, 0, L, vec, gs);
+        load_pos(pr, 0, L, pvec, p);
+        float g[W - 1];
+#pragma unroll
+        for (int t = 0; t < W - 1; ++t) {
+            g[t] = gs[t];
+            if (silu) {
+                const float v = conv_pre<W>(xs, t, p[t], wk, b0);
+                const float sg = sigmoid_f(v);
+                g[t] *= sg * (1.0f + v * (1.0f - sg));
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < W - 1; ++j) {
+            float a = 0.0f;
+#pragma unroll
+            for (int t = 0; t <= j; ++t)
+                if (t - j + W - 1 <= p[t]) a = fmaf(wk[j - t], g[t], a);
+            // a row shorter than W-1 copies initial input j >= L to final input j - L
+            if (st.dxfinal && j >= L) a += Storage<T>::load1(st.dxfinal + row * (W - 1) + (j - L));
+            Storage<TO>::store1(st.dxinit + row * (W - 1) + j, a);
         }
     }
     block_sum<W + 1>(acc, red);
@@ -203,26 +272,34 @@ hipError_t conv_fwd_t(const ConvArgs& a, hipStream_t s) {
     dim3 grid((unsigned)(a.batch * a.dim)), block(kThreads);
     const T* x = static_cast<const T*>(a.x);
     TO* o = static_cast<TO*>(a.out);
+    const ConvStates<T, TO> st{static_cast<const T*>(a.xinit), static_cast<T*>(a.xfinal), nullptr, nullptr};
     switch (a.width) {
-        case 2: hipLaunchKernelGGL((conv1d_fwd_kernel<T, TO, 2>), grid, block, 0, s, x, a.w, a.bias, a.pos, o, a.dim, a.seqlen, a.silu, vec, pvec); break;
-        case 3: hipLaunchKernelGGL((conv1d_fwd_kernel<T, TO, 3>), grid, block, 0, s, x, a.w, a.bias, a.pos, o, a.dim, a.seqlen, a.silu, vec, pvec); break;
-        default: hipLaunchKernelGGL((conv1d_fwd_kernel<T, TO, 4>), grid, block, 0, s, x, a.w, a.bias, a.pos, o, a.dim, a.seqlen, a.silu, vec, pvec); break;
+        case 2: hipLaunchKernelGGL((conv1d_fwd_kernel<T, TO, 2>), grid, block, 0, s, x, a.w, a.bias, a.pos, o, st, a.dim, a.seqlen, a.silu, vec, pvec); break;
+        case 3: hipLaunchKernelGGL((conv1d_fwd_kernel<T, TO, 3>), grid, block, 0, s, x, a.w, a.bias, a.pos, o, st, a.dim, a.seqlen, a.silu, vec, pvec); break;
+        default: hipLaunchKernelGGL((conv1d_fwd_kernel<T, TO, 4>), grid, block, 0, s, x, a.w, a.bias, a.pos, o, st, a.dim, a.seqlen, a.silu, vec, pvec); break;
     }
     return hipGetLastError();
+}
+
+template <typename T, typename TO, int W, bool DXF>
+void conv_bwd_w(const ConvArgs& a, hipStream_t s, int vec, int pvec) {
+    const ConvStates<T, TO> st{static_cast<const T*>(a.xinit), nullptr, static_cast<const T*>(a.dxfinal),
+                               static_cast<TO*>(a.dxinit)};
+    hipLaunchKernelGGL((conv1d_bwd_kernel<T, TO, W, kTokBwd, DXF>), dim3((unsigned)(a.batch * a.dim)),
+                       dim3(kThreads), 0, s, static_cast<const T*>(a.x), a.w, a.bias, a.pos,
+                       static_cast<const T*>(a.dout), static_cast<TO*>(a.out), a.partial, st, a.dim,
+                       a.seqlen, a.silu, vec, pvec);
 }
 
 template <typename T, typename TO>
 hipError_t conv_bwd_t(const ConvArgs& a, hipStream_t s) {
     const int vec = (a.seqlen % Storage<T>::kPerVec) == 0 && (a.seqlen % Storage<TO>::kPerVec) == 0;
     const int pvec = (a.seqlen % 4) == 0;
-    dim3 grid((unsigned)(a.batch * a.dim)), block(kThreads);
-    const T* x = static_cast<const T*>(a.x);
-    const T* g = static_cast<const T*>(a.dout);
-    TO* dx = static_cast<TO*>(a.out);
+    const bool dxf = a.dxfinal != nullptr;
     switch (a.width) {
-        case 2: hipLaunchKernelGGL((conv1d_bwd_kernel<T, TO, 2, kTokBwd>), grid, block, 0, s, x, a.w, a.bias, a.pos, g, dx, a.partial, a.dim, a.seqlen, a.silu, vec, pvec); break;
-        case 3: hipLaunchKernelGGL((conv1d_bwd_kernel<T, TO, 3, kTokBwd>), grid, block, 0, s, x, a.w, a.bias, a.pos, g, dx, a.partial, a.dim, a.seqlen, a.silu, vec, pvec); break;
-        default: hipLaunchKernelGGL((conv1d_bwd_kernel<T, TO, 4, kTokBwd>), grid, block, 0, s, x, a.w, a.bias, a.pos, g, dx, a.partial, a.dim, a.seqlen, a.silu, vec, pvec); break;
+        case 2: dxf ? conv_bwd_w<T, TO, 2, true>(a, s, vec, pvec) : conv_bwd_w<T, TO, 2, false>(a, s, vec, pvec); break;
+        case 3: dxf ? conv_bwd_w<T, TO, 3, true>(a, s, vec, pvec) : conv_bwd_w<T, TO, 3, false>(a, s, vec, pvec); break;
+        default: dxf ? conv_bwd_w<T, TO, 4, true>(a, s, vec, pvec) : conv_bwd_w<T, TO, 4, false>(a, s, vec, pvec); break;
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

@@ -18,6 +18,11 @@ struct ConvArgs {
     float* dw;          // bwd only
     float* dbias;       // bwd only
     float* partial;     // bwd only: (batch*dim, width+1)
+    // state passing across rows, each (batch, dim, width-1) or null
+    const void* xinit;  // inputs before the row (x's dtype)
+    void* xfinal;       // fwd: the row's last width-1 inputs (x's dtype)
+    const void* dxfinal;// bwd: gradient of xfinal (dout's dtype)
+    void* dxinit;       // bwd: gradient of xinit (dx's dtype)
     int64_t batch, dim, seqlen;
     int32_t width, dtype, silu;
 };
@@ -36,6 +41,11 @@ struct ScanArgs {
     const float* delta_bias;
     const int32_t* pos;
     int32_t softplus;
+    // state passing across rows, each (batch, dim, dstate) fp32 or null
+    const float* h0;        // state before the row
+    float* hfinal;          // fwd: state after the row
+    const float* dhfinal;   // bwd: gradient of hfinal
+    float* dh0;             // bwd: gradient of h0
     // forward
     void* out;
     float* states;          // (batch, dim, nchunk, dstate); written by fwd, read by bwd
@@ -84,7 +94,7 @@ inline SegPlan scan_segments(int64_t batch, int64_t dim, int64_t seqlen) {
 
 hipError_t launch_scan_fwd(const ScanArgs& a, hipStream_t s);
 hipError_t launch_scan_bwd(const ScanArgs& a, hipStream_t s);
-hipError_t launch_check_pos(const int32_t* pos, int64_t batch, int64_t seqlen, int32_t* flag,
-                            hipStream_t s);
+hipError_t launch_check_pos(const int32_t* pos, int64_t batch, int64_t seqlen, int32_t continued,
+                            int32_t* flag, hipStream_t s);
 
 }  // namespace pm

@@ -63,6 +63,9 @@ struct BwdParams {
     const int32_t* pos;
     const void* dout;
     const float* states;
+    const float* h0;      // state before each row (batch, dim, kN), or null
+    const float* dhfinal; // gradient of the state after each row, or null
+    float* dh0;           // gradient of h0, or null
     void* du;
     void* ddelta;
     void* dz;
@@ -140,8 +143,14 @@ void scan_bwd_kernel(BwdParams p) {
         const int64_t dd = min((int64_t)g * kRows + rr, p.dim - 1);
         const float A2n = p.A[dd * kN + n] * kLog2e;
         sm.A2[rr][n] = A2n;
-        sm.xc[rr][n] = p.xc_in ? p.xc_in[((b * p.dim + dd) * p.nseg + seg) * kN + n] : 0.0f;
-        sm.an[rr][n] = c1 < nchunk ? fast_exp2(fmaf(dt_next, A2n, m_next)) : 0.0f;
+        // at the row end the carry is the final state's gradient, entering h_{L-1} with
+        // multiplier 1
+        const bool row_end = c1 == nchunk;
+        float xc0 = 0.0f;
+        if (p.xc_in) xc0 = p.xc_in[((b * p.dim + dd) * p.nseg + seg) * kN + n];
+        else if (row_end && p.dhfinal) xc0 = p.dhfinal[(b * p.dim + dd) * kN + n];
+        sm.xc[rr][n] = xc0;
+        sm.an[rr][n] = !row_end ? fast_exp2(fmaf(dt_next, A2n, m_next)) : (p.dhfinal ? 1.0f : 0.0f);
         sm.dA[rr][n] = 0.0f;
     }
     // One chunk; FULL (block-uniform) means the chunk lies inside the row and vector
@@ -167,7 +176,8 @@ void scan_bwd_kernel(BwdParams p) {
         {   // state at the chunk start (h after token lb-1), saved by the forward
             const int rr = tid >> 4, n = tid & 15;
             const int64_t dd = min((int64_t)g * kRows + rr, p.dim - 1);
-            sm.hin[rr][n] = c > 0 ? p.states[((b * p.dim + dd) * p.nchunk_states + (c - 1)) * kN + n] : 0.0f;
+            sm.hin[rr][n] = c > 0 ? p.states[((b * p.dim + dd) * p.nchunk_states + (c - 1)) * kN + n]
+                                  : (p.h0 ? p.h0[(b * p.dim + dd) * kN + n] : 0.0f);
         }
         __syncthreads();
 
@@ -381,6 +391,13 @@ void scan_bwd_kernel(BwdParams p) {
     // ---- per-channel partials ----
     dDacc = row_sum_to_15(dDacc);
     dbacc = row_sum_to_15(dbacc);
+    // gradient of the initial state: dh at token 0 times Abar at token 0 (0 at a start),
+    // both left in LDS by lane 0 after the first chunk
+    if (p.dh0 && c0 == 0) {
+        const int rr = tid >> 4, n = tid & 15;
+        const int64_t dd = g * kRows + rr;
+        if (dd < p.dim) p.dh0[(b * p.dim + dd) * kN + n] = sm.an[rr][n] * sm.xc[rr][n];
+    }
     float* pcb = p.part_chan + (b * p.nseg + seg) * p.dim * (kN + 2);
     if (active && j == 15) {
         float* pc = pcb + d * (kN + 2);
@@ -569,14 +586,15 @@ __global__ __launch_bounds__(kThreads) void scan_bwd_agg_kernel(BwdParams p) {
     }
 }
 
-// Chains the segment maps from the row end: xc[s] = dh at the first token of segment s+1.
+// Chains the segment maps from the row end: xc[s] = dh at the first token of segment
+// s+1 (the final state's gradient, or 0, for the last segment).
 __global__ void scan_bwd_carry_kernel(const float* __restrict__ agg, float* __restrict__ xc,
-                                      int64_t rows_n, int nseg) {
+                                      const float* __restrict__ dhfinal, int64_t rows_n, int nseg) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;   // over batch*dim*kN
     if (i >= rows_n) return;
     const int64_t bd = i / kN;
     const int n = (int)(i - bd * kN);
-    float x = 0.0f;
+    float x = dhfinal ? dhfinal[i] : 0.0f;
     for (int s = nseg - 1; s >= 0; --s) {
         const int64_t o = (bd * nseg + s) * kN + n;
         xc[o] = x;
@@ -633,6 +651,7 @@ hipError_t launch_t(const ScanArgs& a, hipStream_t s) {
     BwdParams p;
     p.u = a.u; p.delta = a.delta; p.A = a.A; p.B = a.B; p.C = a.C; p.D = a.D; p.z = a.z;
     p.delta_bias = a.delta_bias; p.pos = a.pos; p.dout = a.dout; p.states = a.states;
+    p.h0 = a.h0; p.dhfinal = a.dhfinal; p.dh0 = a.dh0;
     p.du = a.du; p.ddelta = a.ddelta; p.dz = a.dz; p.part_bc = a.part_bc; p.part_chan = a.part_chan;
     p.dim = a.dim; p.L = a.seqlen;
     p.nchunk_states = (int)((a.seqlen + kCH - 1) / kCH);
@@ -653,7 +672,7 @@ hipError_t launch_t(const ScanArgs& a, hipStream_t s) {
         if (e != hipSuccess) return e;
         const int64_t rows_n = a.batch * a.dim * kN;
         hipLaunchKernelGGL(scan_bwd_carry_kernel, dim3((unsigned)((rows_n + 255) / 256)), dim3(256), 0, s,
-                           a.ws_agg, a.ws_carry, rows_n, p.nseg);
+                           a.ws_agg, a.ws_carry, a.dhfinal, rows_n, p.nseg);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
         p.xc_in = a.ws_carry;

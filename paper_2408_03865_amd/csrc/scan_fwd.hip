@@ -59,6 +59,8 @@ struct FwdParams {
     const int32_t* pos;
     void* out;
     float* states;
+    const float* h0;          // state before each row (batch, dim, kN), or null
+    float* hfinal;            // state after each row (batch, dim, kN), or null
     float* agg;               // aggregate pass output: (batch, dim, nseg, kN, 2) = (P, H)
     const float* carry_in;    // main pass: state before each segment (batch, dim, nseg, kN), or null
     int64_t dim, L;
@@ -100,7 +102,12 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_kernel(FwdParams p) {
         const int rr = tid >> 4, n = tid & 15;
         const int64_t dd = min((int64_t)blockIdx.x * kRows + rr, p.dim - 1);
         sm.A2[rr][n] = p.A[dd * kN + n] * kLog2e;
-        sm.carry[rr][n] = (!AGG && p.carry_in) ? p.carry_in[((b * p.dim + dd) * p.nseg + seg) * kN + n] : 0.0f;
+        float c0v = 0.0f;
+        if (!AGG) {
+            if (p.carry_in) c0v = p.carry_in[((b * p.dim + dd) * p.nseg + seg) * kN + n];
+            else if (p.h0) c0v = p.h0[(b * p.dim + dd) * kN + n];
+        }
+        sm.carry[rr][n] = c0v;
         sm.pseg[rr][n] = 1.0f;
     }
     const float Dd = p.D ? p.D[d] : 0.0f;
@@ -241,17 +248,24 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_kernel(FwdParams p) {
             o[0] = sm.pseg[rr][n];
             o[1] = sm.carry[rr][n];
         }
+    } else if (p.hfinal && c1 == nchunk) {
+        // the carry after the row's last chunk is h after its last token (tokens past
+        // the row end are identities)
+        const int rr = tid >> 4, n = tid & 15;
+        const int64_t dd = (int64_t)blockIdx.x * kRows + rr;
+        if (dd < p.dim) p.hfinal[(b * p.dim + dd) * kN + n] = sm.carry[rr][n];
     }
 }
 
-// Chains the segment maps along each row: carry[s] = state after segment s-1.
+// Chains the segment maps along each row: carry[s] = state after segment s-1 (the
+// row's initial state, or 0, for s = 0).
 __global__ void scan_fwd_carry_kernel(const float* __restrict__ agg, float* __restrict__ carry,
-                                      int64_t rows_n, int nseg) {
+                                      const float* __restrict__ h0, int64_t rows_n, int nseg) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;   // over batch*dim*kN
     if (i >= rows_n) return;
     const int64_t bd = i / kN;
     const int n = (int)(i - bd * kN);
-    float h = 0.0f;
+    float h = h0 ? h0[i] : 0.0f;
     for (int s = 0; s < nseg; ++s) {
         const int64_t o = (bd * nseg + s) * kN + n;
         carry[o] = h;
@@ -264,6 +278,7 @@ hipError_t launch_t(const ScanArgs& a, hipStream_t s) {
     FwdParams p;
     p.u = a.u; p.delta = a.delta; p.A = a.A; p.B = a.B; p.C = a.C; p.D = a.D; p.z = a.z;
     p.delta_bias = a.delta_bias; p.pos = a.pos; p.out = a.out; p.states = a.states;
+    p.h0 = a.h0; p.hfinal = a.hfinal;
     p.dim = a.dim; p.L = a.seqlen;
     p.nchunk_states = (int)((a.seqlen + kStride - 1) / kStride);
     p.softplus = a.softplus;
@@ -283,7 +298,7 @@ hipError_t launch_t(const ScanArgs& a, hipStream_t s) {
         if (e != hipSuccess) return e;
         const int64_t rows_n = a.batch * a.dim * kN;
         hipLaunchKernelGGL(scan_fwd_carry_kernel, dim3((unsigned)((rows_n + 255) / 256)), dim3(256), 0, s,
-                           a.ws_agg, a.ws_carry, rows_n, p.nseg);
+                           a.ws_agg, a.ws_carry, a.h0, rows_n, p.nseg);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
         p.carry_in = a.ws_carry;

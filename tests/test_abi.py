@@ -26,7 +26,7 @@ def test_exports_every_declared_symbol():
     lib = _lib()
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.packmamba_abi_version() == 2
+    assert lib.packmamba_abi_version() == 3
 
 
 def test_status_strings():
@@ -87,46 +87,62 @@ def test_argument_errors_before_launch():
     P = 0x10000          # fake, aligned; every case below must fail validation first
     U = 0x10008          # fake, misaligned
     conv = lib.packmamba_causal_conv1d_fwd
-    assert conv(None, P, None, P, P, 1, 1, 8, 4, 0, 1, None) == 1           # x NULL
-    assert conv(P, P, None, P, P, 0, 1, 8, 4, 0, 1, None) == 2              # batch 0
-    assert conv(P, P, None, P, P, 1, 1, -3, 4, 0, 1, None) == 2             # seqlen < 0
-    assert conv(P, P, None, P, P, 1, 1, 1 << 40, 4, 0, 1, None) == 2        # too large
-    assert conv(P, P, None, P, P, 1, 1, 8, 5, 0, 1, None) == 3              # width 5
-    assert conv(P, P, None, P, P, 1, 1, 8, 1, 0, 1, None) == 3              # width 1
-    assert conv(P, P, None, P, P, 1, 1, 8, 4, 7, 1, None) == 3              # dtype
-    assert conv(U, P, None, P, P, 1, 1, 8, 4, 0, 1, None) == 4              # misaligned x
+    # x, w, bias, pos, initial_x, out, final_x, batch, dim, seqlen, width, dtype, silu, stream
+    assert conv(None, P, None, P, None, P, None, 1, 1, 8, 4, 0, 1, None) == 1     # x NULL
+    assert conv(P, P, None, P, None, P, None, 0, 1, 8, 4, 0, 1, None) == 2        # batch 0
+    assert conv(P, P, None, P, None, P, None, 1, 1, -3, 4, 0, 1, None) == 2       # seqlen < 0
+    assert conv(P, P, None, P, None, P, None, 1, 1, 1 << 40, 4, 0, 1, None) == 2  # too large
+    assert conv(P, P, None, P, None, P, None, 1, 1, 8, 5, 0, 1, None) == 3        # width 5
+    assert conv(P, P, None, P, None, P, None, 1, 1, 8, 1, 0, 1, None) == 3        # width 1
+    assert conv(P, P, None, P, None, P, None, 1, 1, 8, 4, 7, 1, None) == 3        # dtype
+    assert conv(U, P, None, P, None, P, None, 1, 1, 8, 4, 0, 1, None) == 4        # misaligned x
+    assert conv(P, P, None, P, U, P, None, 1, 1, 8, 4, 0, 1, None) == 4           # misaligned initial_x
     cbwd = lib.packmamba_causal_conv1d_bwd
-    assert cbwd(P, P, P, P, P, P, P, None, P, 1 << 20, 1, 1, 8, 4, 0, 1, None) == 1   # bias without dbias
-    assert cbwd(P, P, None, P, P, P, P, None, P, 1, 1, 1, 8, 4, 0, 1, None) == 5      # workspace small
-    assert cbwd(P, P, None, P, P, P, P, None, None, 1 << 20, 1, 1, 8, 4, 0, 1, None) == 5
+    # x, w, bias, pos, initial_x, dout, dfinal_x, dx, dw, dbias, dinitial_x, ws, ws_bytes, ...
+    assert cbwd(P, P, P, P, None, P, None, P, P, None, None, P, 1 << 20, 1, 1, 8, 4, 0, 1, None) == 1  # bias without dbias
+    assert cbwd(P, P, None, P, P, P, None, P, P, None, None, P, 1 << 20, 1, 1, 8, 4, 0, 1, None) == 1  # initial_x without dinitial_x
+    assert cbwd(P, P, None, P, None, P, None, P, P, None, P, P, 1 << 20, 1, 1, 8, 4, 0, 1, None) == 1  # dinitial_x without initial_x
+    assert cbwd(P, P, None, P, None, P, None, P, P, None, None, P, 1, 1, 1, 8, 4, 0, 1, None) == 5     # workspace small
+    assert cbwd(P, P, None, P, None, P, None, P, P, None, None, None, 1 << 20, 1, 1, 8, 4, 0, 1, None) == 5
     fwd = lib.packmamba_selective_scan_fwd
-    args = [P, P, P, P, P, None, None, None, 1, P, P, None, None, 0, 1, 1, 8, 16, 1, None]
+    # u, delta, A, B, C, D, z, delta_bias, softplus, pos, initial_state, out, final_state, states,
+    # ws, ws_bytes, batch, dim, seqlen, dstate, dtype, stream
+    args = [P, P, P, P, P, None, None, None, 1, P, None, P, None, None, None, 0, 1, 1, 8, 16, 1, None]
     a = list(args); a[0] = None
     assert fwd(*a) == 1
-    a = list(args); a[10] = None                                            # no out and no states
+    a = list(args); a[11] = None                                            # no out, states or final state
     assert fwd(*a) == 1
-    a = list(args); a[17] = 8                                               # dstate 8
+    a = list(args); a[19] = 8                                               # dstate 8
     assert fwd(*a) == 3
     a = list(args); a[6] = U                                                # misaligned z
     assert fwd(*a) == 4
-    a = list(args); a[14] = 70000                                           # batch too large
+    a = list(args); a[12] = U                                               # misaligned final_state
+    assert fwd(*a) == 4
+    a = list(args); a[16] = 70000                                           # batch too large
     assert fwd(*a) == 2
-    a = list(args); a[15] = 16; a[16] = 65536                               # split rows need a workspace
+    a = list(args); a[17] = 16; a[18] = 65536                               # split rows need a workspace
     assert fwd(*a) == 5
-    a[12] = P; a[13] = 64
+    a[14] = P; a[15] = 64
     assert fwd(*a) == 5
-    a[12] = U; a[13] = 1 << 30
+    a[14] = U; a[15] = 1 << 30
     assert fwd(*a) == 4
     bwd = lib.packmamba_selective_scan_bwd
-    bargs = [P, P, P, P, P, P, None, None, 1, P, P, None, P, P, P, P, P, P, None, None, P, 1 << 40,
-             1, 1, 8, 16, 1, None]
-    a = list(bargs); a[17] = None                                           # D without dD
+    # u, delta, A, B, C, D, z, delta_bias, softplus, pos, initial_state, dout, dfinal_state, states,
+    # du, ddelta, dA, dB, dC, dD, dz, ddelta_bias, dinitial_state, ws, ws_bytes, batch, dim, seqlen,
+    # dstate, dtype, stream
+    bargs = [P, P, P, P, P, P, None, None, 1, P, None, P, None, None, P, P, P, P, P, P, None, None, None,
+             P, 1 << 40, 1, 1, 8, 16, 1, None]
+    a = list(bargs); a[19] = None                                           # D without dD
     assert bwd(*a) == 1
-    a = list(bargs); a[18] = P                                              # dz without z
+    a = list(bargs); a[20] = P                                              # dz without z
     assert bwd(*a) == 1
-    a = list(bargs); a[21] = 16                                             # workspace too small
+    a = list(bargs); a[10] = P                                              # initial_state without its gradient
+    assert bwd(*a) == 1
+    a = list(bargs); a[22] = P                                              # dinitial_state without initial_state
+    assert bwd(*a) == 1
+    a = list(bargs); a[24] = 16                                             # workspace too small
     assert bwd(*a) == 5
-    a = list(bargs); a[25] = 32
+    a = list(bargs); a[28] = 32
     assert bwd(*a) == 3
-    assert lib.packmamba_check_position_indices(None, 1, 8, P, None) == 1
-    assert lib.packmamba_check_position_indices(U, 1, 8, P, None) == 4
+    assert lib.packmamba_check_position_indices(None, 1, 8, 0, P, None) == 1
+    assert lib.packmamba_check_position_indices(U, 1, 8, 1, P, None) == 4
