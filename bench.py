@@ -92,7 +92,9 @@ class Chain:
     -> scan bwd -> conv bwd (upstream gradient = the scan's du).  Every buffer,
     workspaces included, is allocated here, before any timing."""
 
-    def __init__(self, lib, t, code, width, stream):
+    def __init__(self, lib, t, code, width, stream, states=False):
+        """states: every row continues a sequence from another row (its first position
+        index is not 0): initial states go in, final states come out, with gradients."""
         import torch
         from paper_2408_03865_amd import _lib
         self.lib, self.t, self.code, self.W, self.sp = lib, t, code, width, stream.cuda_stream
@@ -114,34 +116,44 @@ class Chain:
         self.ws_fwd = ws(lib.packmamba_selective_scan_fwd_workspace_size(Nb, Dn, L, N))
         self.ws_scan = ws(lib.packmamba_selective_scan_bwd_workspace_size(Nb, Dn, L, N))
         self.ws_conv = ws(lib.packmamba_causal_conv1d_bwd_workspace_size(Nb, Dn, L, width))
+        self.st = {}
+        if states:
+            g = torch.Generator(device=dev).manual_seed(7)
+            xs = lambda: torch.randn((Nb, Dn, width - 1), generator=g, device=dev).to(x.dtype)  # noqa: E731
+            hs = lambda: torch.randn((Nb, Dn, N), generator=g, device=dev)  # noqa: E731
+            self.st = {"xi": xs(), "xf": xs(), "dxf": xs(), "dxi": xs(), "h0": hs(), "hf": hs(),
+                       "dhf": hs(), "dh0": hs()}
 
     def ops(self):
         from paper_2408_03865_amd import _lib
         lib, t, c, sp = self.lib, self.t, self.code, self.sp
         Nb, Dn, L, N, W = self.Nb, self.Dn, self.L, self.N, self.W
         P = lambda v: v.data_ptr()  # noqa: E731
+        S = lambda k: self.st[k].data_ptr() if self.st else None  # noqa: E731
 
         def conv_fwd():
             _lib.check("conv_fwd", lib.packmamba_causal_conv1d_fwd(
-                P(t["x"]), P(t["w"]), P(t["bias"]), P(t["pos"]), None, P(self.u), None, Nb, Dn, L, W, c, 1, sp))
+                P(t["x"]), P(t["w"]), P(t["bias"]), P(t["pos"]), S("xi"), P(self.u), S("xf"), Nb, Dn, L, W,
+                c, 1, sp))
 
         def scan_fwd():
             _lib.check("scan_fwd", lib.packmamba_selective_scan_fwd(
                 P(self.u), P(t["delta"]), P(t["A"]), P(t["B"]), P(t["C"]), P(t["D"]), P(t["z"]),
-                P(t["delta_bias"]), 1, P(t["pos"]), None, P(self.out), None, P(self.states),
+                P(t["delta_bias"]), 1, P(t["pos"]), S("h0"), P(self.out), S("hf"), P(self.states),
                 P(self.ws_fwd), self.ws_fwd.numel(), Nb, Dn, L, N, c, sp))
 
         def scan_bwd():
             _lib.check("scan_bwd", lib.packmamba_selective_scan_bwd(
                 P(self.u), P(t["delta"]), P(t["A"]), P(t["B"]), P(t["C"]), P(t["D"]), P(t["z"]),
-                P(t["delta_bias"]), 1, P(t["pos"]), None, P(t["dout"]), None, P(self.states),
+                P(t["delta_bias"]), 1, P(t["pos"]), S("h0"), P(t["dout"]), S("dhf"), P(self.states),
                 P(self.du), P(self.ddl), P(self.dA), P(self.dB), P(self.dC), P(self.dD), P(self.dz),
-                P(self.ddb), None, P(self.ws_scan), self.ws_scan.numel(), Nb, Dn, L, N, c, sp))
+                P(self.ddb), S("dh0"), P(self.ws_scan), self.ws_scan.numel(), Nb, Dn, L, N, c, sp))
 
         def conv_bwd():
             _lib.check("conv_bwd", lib.packmamba_causal_conv1d_bwd(
-                P(t["x"]), P(t["w"]), P(t["bias"]), P(t["pos"]), None, P(self.du), None, P(self.dx), P(self.dw),
-                P(self.dcb), None, P(self.ws_conv), self.ws_conv.numel(), Nb, Dn, L, W, c, 1, sp))
+                P(t["x"]), P(t["w"]), P(t["bias"]), P(t["pos"]), S("xi"), P(self.du), S("dxf"), P(self.dx),
+                P(self.dw), P(self.dcb), S("dxi"), P(self.ws_conv), self.ws_conv.numel(), Nb, Dn, L, W, c, 1,
+                sp))
 
         return [("conv_fwd", conv_fwd), ("scan_fwd", scan_fwd), ("scan_bwd", scan_bwd),
                 ("conv_bwd", conv_bwd)]
@@ -155,6 +167,39 @@ def sequences(pos):
         st = np.flatnonzero(pos[b] == 0).tolist() + [pos.shape[1]]
         out += [(b, st[i], st[i + 1] - st[i]) for i in range(len(st) - 1)]
     return out
+
+
+def time_steps(step_fn, stream, steps, warmup):
+    import torch
+    for _ in range(warmup):
+        step_fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(steps):
+        step_fn()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps
+
+
+def with_states(lib, tens, pos_host, code, width, stream, steps, warmup, packed_ms):
+    """The same step with every row continuing a sequence cut at the end of another row
+    (its first sequence's position indices start at 100), initial states in, final
+    states out, and their gradients: the state-passing path."""
+    import numpy as np
+    import torch
+    pos = pos_host.copy()
+    for b in range(pos.shape[0]):
+        st = np.flatnonzero(pos[b, 1:] == 0)
+        n = int(st[0]) + 1 if st.size else pos.shape[1]
+        pos[b, :n] += 100
+    t = dict(tens, pos=torch.from_numpy(pos).to(tens["x"].device))
+    ch = Chain(lib, t, code, width, stream, states=True)
+    ops = [f for _, f in ch.ops()]
+    ms = time_steps(lambda: [f() for f in ops], stream, steps, warmup)
+    return {"ms_per_step": round(ms, 4), "overhead_vs_packed": round(ms / packed_ms - 1.0, 4),
+            "rows_continued": int(pos.shape[0])}
 
 
 def comparison(lib, tens, pos_host, code, width, stream, steps, warmup, packed_ms):
@@ -221,6 +266,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="2")
     ap.add_argument("--variant", default="paper", choices=["paper", "general"])
+    ap.add_argument("--dtype", default=None, choices=["f32", "bf16"],
+                    help="storage type of the activations, overriding the workload's (bf16 at the large shapes)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-compare", action="store_true",
                     help="skip the padded / single-sequence runs of the same tokens (Mamba-1.4B shape only)")
@@ -255,7 +302,7 @@ def main():
         __graft_entry__.build()
     lib = _lib.load()
     dev = torch.device("cuda:0")
-    cfg = W.config(args.config)
+    cfg = W.config(args.config, **({"dtype": args.dtype} if args.dtype else {}))
     Nb, Dn, L, N, Wd = cfg.batch, cfg.dim, cfg.seqlen, cfg.dstate, cfg.width
     code = _lib.BF16 if cfg.dtype == "bf16" else _lib.F32
     tdt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
@@ -350,6 +397,9 @@ def main():
         "device": torch.cuda.get_device_name(0),
     }
     if args.config == "2" and not args.no_compare:
+        print("# state passing: every row continues a sequence", file=sys.stderr, flush=True)
+        line["state_passing"] = with_states(lib, tens, d["pos"], code, Wd, stream, steps=10, warmup=2,
+                                            packed_ms=ms_step)
         print("# comparison: padded and single-sequence runs of the same tokens", file=sys.stderr, flush=True)
         line["comparison"] = comparison(lib, tens, d["pos"], code, Wd, stream, steps=5, warmup=2,
                                         packed_ms=ms_step)

@@ -70,6 +70,21 @@ def test_parity_full_size_sampled(key):
     compare(r32, refc, TOL["bf16"], PER_TOKEN + PER_CHANNEL, sl_d=chans, label=f"cfg{key} chans ")
 
 
+@pytest.mark.slow
+def test_parity_f32_full_size_sampled():
+    """fp32 inputs at the Mamba-1.4B shape (8 x 4096 x 4096): batch row 0 in full and 16
+    channels on every row, against the fp32 bound."""
+    cfg = W.config("2", dtype="f32")
+    note(f"parity full-size fp32 {cfg}")
+    d = W.make_inputs(cfg)
+    r = run_gpu(gpu_inputs(d, "f32"))
+    ref0 = oracle_run(d, sl_b=slice(0, 1))
+    compare(r, ref0, TOL["f32"], PER_TOKEN + PER_B, sl_b=slice(0, 1), label="cfg2 f32 row0 ")
+    chans = np.unique(np.linspace(0, cfg.dim - 1, 16).astype(int))
+    refc = oracle_run(d, sl_d=chans)
+    compare(r, refc, TOL["f32"], PER_TOKEN + PER_CHANNEL, sl_d=chans, label="cfg2 f32 chans ")
+
+
 def test_saved_states_match_oracle():
     import oracle as O
     cfg = W.config("1", dim=48, seqlen=1000)
