@@ -202,6 +202,22 @@ def with_states(lib, tens, pos_host, code, width, stream, steps, warmup, packed_
             "rows_continued": int(pos.shape[0])}
 
 
+def packing_rates(law, seqlen, count=20000, seed=0):
+    """Padding of the host packing plans (the library's C++ planner) on a stream of
+    ``count`` lengths drawn from the workload's length law: the sequential seal, local
+    greedy with windows of 64 and 1024 sequences, and cutting at the row end."""
+    import numpy as np
+    import paper_2408_03865_amd as P
+    import workloads as W
+    ln = W.draw_stream_lengths(law, np.random.default_rng(seed), count)
+    out = {"sequences": count, "mean_length": round(float(ln.mean()), 1)}
+    for name, policy, w in (("sequential", "sequential", 1), ("greedy64", "greedy", 64),
+                            ("greedy1024", "greedy", 1024), ("cut", "cut", 1)):
+        pieces, rows = P.pack_plan(ln, seqlen, policy, window=w)
+        out[name] = round(P.padding_rate(pieces, rows, seqlen), 5)
+    return out
+
+
 def comparison(lib, tens, pos_host, code, width, stream, steps, warmup, packed_ms):
     """The same real tokens and kernels without packing: (a) padded, one sequence per row
     padded with zeros to the longest length, position indices 0..L-1 on every row; (b)
@@ -403,6 +419,8 @@ def main():
         print("# comparison: padded and single-sequence runs of the same tokens", file=sys.stderr, flush=True)
         line["comparison"] = comparison(lib, tens, d["pos"], code, Wd, stream, steps=5, warmup=2,
                                         packed_ms=ms_step)
+    if cfg.lengths[0] == "lognormal":
+        line["packing_padding"] = packing_rates(cfg.lengths, L)
     if not args.no_cpu_baseline:
         print("# cpu baseline (oracle)", file=sys.stderr, flush=True)
         line["cpu_baseline"] = cpu_baseline(d, cfg, args.cpu_rows)

@@ -212,6 +212,52 @@ int packmamba_check_position_indices(const int32_t* position_indices, int64_t ba
                                      int64_t seqlen, int32_t continued, int32_t* d_flag,
                                      void* stream);
 
+/*
+ * Host-side packing plans (§3.1, §5).  Plain CPU functions on host memory: they
+ * enqueue nothing and need no GPU.
+ *
+ * A plan places each sequence of a stream (lengths[i] tokens, in received order)
+ * into rows of `seqlen` tokens as one or more pieces.  Policies:
+ *   PACKMAMBA_PACK_SEQUENTIAL  in order; a sequence that does not fit the rest of
+ *       the current row seals it, the rest being padding (§3.1, §5).  Sequences
+ *       longer than a row are truncated to a row.
+ *   PACKMAMBA_PACK_GREEDY      local greedy with a partial sort (§5): windows of
+ *       `window` sequences, each sorted longest first and placed first-fit into
+ *       the rows opened for that window, which are sealed when it ends.
+ *       Truncates like the sequential policy.
+ *   PACKMAMBA_PACK_CUT         the future work of §5: rows are filled to the end, a
+ *       sequence that does not fit is cut at the row end and continues in the next
+ *       row (first_pos > 0), so only the last row holds padding.  The operators'
+ *       state passing makes this exact.
+ * pieces: NULL to query the sizes (n_pieces, n_rows), else room for max_pieces
+ * (PACKMAMBA_ERR_WORKSPACE if too few).  Errors: ERR_NULL, ERR_SHAPE (a length
+ * <= 0, seqlen <= 0, window <= 0 for the greedy policy), ERR_UNSUPPORTED (policy).
+ */
+#define PACKMAMBA_PACK_SEQUENTIAL 0
+#define PACKMAMBA_PACK_GREEDY 1
+#define PACKMAMBA_PACK_CUT 2
+
+typedef struct {
+    int64_t seq;        /* index of the sequence in the stream */
+    int64_t row;        /* row it is placed in */
+    int64_t offset;     /* first token of the piece inside the row */
+    int64_t length;     /* tokens in the piece */
+    int64_t first_pos;  /* position of the piece's first token inside its sequence */
+} packmamba_piece;
+
+int packmamba_pack_plan(const int64_t* lengths, int64_t count, int64_t seqlen, int32_t policy,
+                        int64_t window, packmamba_piece* pieces, int64_t max_pieces,
+                        int64_t* n_pieces, int64_t* n_rows);
+
+/*
+ * Position indices (§3.1) of a plan, written to a host int32 array
+ * (n_rows, seqlen): each piece gets first_pos, first_pos+1, ...; padding tokens get
+ * index 0 (each its own sequence, so they affect nothing).  Rows that begin with a
+ * piece whose first_pos > 0 continue a sequence (see state passing above).
+ */
+int packmamba_pack_positions(const packmamba_piece* pieces, int64_t n_pieces, int64_t n_rows,
+                             int64_t seqlen, int32_t* position_indices);
+
 #ifdef __cplusplus
 }
 #endif

@@ -30,7 +30,8 @@ from ._lib import BF16, BF16_F32OUT, F32, STATE_STRIDE, PackMambaError, load
 
 __all__ = [
     "causal_conv1d_fwd", "causal_conv1d_bwd", "selective_scan_fwd", "selective_scan_bwd",
-    "check_position_indices", "saved_states_size", "segments", "PackMambaError", "load", "F32", "BF16",
+    "check_position_indices", "saved_states_size", "segments", "pack_plan", "pack_positions",
+    "padding_rate", "PackMambaError", "load", "F32", "BF16",
     "STATE_STRIDE", "BF16_F32OUT",
 ]
 
@@ -188,3 +189,44 @@ def check_position_indices(position_indices, continued: bool = False) -> bool:
                                                  _stream(position_indices))
     _lib.check("packmamba_check_position_indices", st)
     return int(flag[0].item()) == 0
+
+
+_POLICIES = {"sequential": _lib.PACK_SEQUENTIAL, "greedy": _lib.PACK_GREEDY, "cut": _lib.PACK_CUT}
+
+
+def pack_plan(lengths, seqlen: int, policy: str = "sequential", window: int = 64):
+    """Host packing plan of a stream of sequence lengths (the library's C++ planner):
+    returns (pieces, n_rows), pieces an int64 array (n, 5) of (seq, row, offset,
+    length, first_pos).  Policies: "sequential" (seal a row when the next sequence
+    does not fit), "greedy" (windows of ``window`` sequences sorted longest first,
+    first-fit), "cut" (rows filled to the end, sequences cut and continued in the
+    next row; needs the operators' state passing)."""
+    import ctypes
+    import numpy as np
+    lib = load()
+    ln = np.ascontiguousarray(lengths, dtype=np.int64)
+    n_pieces, n_rows = ctypes.c_int64(), ctypes.c_int64()
+    pol = _POLICIES[policy]
+    _lib.check("packmamba_pack_plan", lib.packmamba_pack_plan(
+        ln.ctypes.data, ln.size, seqlen, pol, window, None, 0, ctypes.byref(n_pieces), ctypes.byref(n_rows)))
+    out = np.zeros((n_pieces.value, 5), dtype=np.int64)
+    _lib.check("packmamba_pack_plan", lib.packmamba_pack_plan(
+        ln.ctypes.data, ln.size, seqlen, pol, window, out.ctypes.data, n_pieces.value,
+        ctypes.byref(n_pieces), ctypes.byref(n_rows)))
+    return out, int(n_rows.value)
+
+
+def pack_positions(pieces, n_rows: int, seqlen: int):
+    """Host int32 position indices (n_rows, seqlen) of a plan (padding tokens get 0)."""
+    import numpy as np
+    pc = np.ascontiguousarray(pieces, dtype=np.int64)
+    pos = np.empty((n_rows, seqlen), dtype=np.int32)
+    _lib.check("packmamba_pack_positions", load().packmamba_pack_positions(
+        pc.ctypes.data if pc.size else None, pc.shape[0], n_rows, seqlen, pos.ctypes.data))
+    return pos
+
+
+def padding_rate(pieces, n_rows: int, seqlen: int) -> float:
+    """Fraction of the rows' tokens that hold no sequence."""
+    import numpy as np
+    return 1.0 - float(np.asarray(pieces)[:, 3].sum()) / float(max(1, n_rows * seqlen))

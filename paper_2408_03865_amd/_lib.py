@@ -27,8 +27,16 @@ EXPORTS = (
     "packmamba_causal_conv1d_bwd", "packmamba_selective_scan_fwd_saved_states_size",
     "packmamba_selective_scan_fwd_workspace_size", "packmamba_selective_scan_fwd",
     "packmamba_selective_scan_bwd_workspace_size", "packmamba_selective_scan_bwd",
-    "packmamba_check_position_indices",
+    "packmamba_check_position_indices", "packmamba_pack_plan", "packmamba_pack_positions",
 )
+
+PACK_SEQUENTIAL, PACK_GREEDY, PACK_CUT = 0, 1, 2
+
+
+class Piece(ctypes.Structure):
+    """packmamba_piece: one sequence's piece in a packing plan."""
+    _fields_ = [("seq", ctypes.c_int64), ("row", ctypes.c_int64), ("offset", ctypes.c_int64),
+                ("length", ctypes.c_int64), ("first_pos", ctypes.c_int64)]
 
 
 class PackMambaError(RuntimeError):
@@ -65,7 +73,10 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.packmamba_selective_scan_bwd_workspace_size.restype = sz
     lib.packmamba_selective_scan_bwd.argtypes = ([vp] * 8 + [i32] + [vp] * 15 + [sz, i64, i64, i64, i32, i32, vp])
     lib.packmamba_check_position_indices.argtypes = [vp, i64, i64, i32, vp, vp]
-    for name in ("packmamba_causal_conv1d_fwd", "packmamba_causal_conv1d_bwd",
+    lib.packmamba_pack_plan.argtypes = [vp, i64, i64, i32, i64, vp, i64, vp, vp]
+    lib.packmamba_pack_positions.argtypes = [vp, i64, i64, i64, vp]
+    for name in ("packmamba_pack_plan", "packmamba_pack_positions", "packmamba_causal_conv1d_fwd",
+                 "packmamba_causal_conv1d_bwd",
                  "packmamba_selective_scan_fwd", "packmamba_selective_scan_bwd",
                  "packmamba_check_position_indices"):
         getattr(lib, name).restype = ctypes.c_int

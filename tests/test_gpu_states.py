@@ -162,3 +162,38 @@ def test_check_position_indices_continued():
     assert P.check_position_indices(t, continued=True)
     pos[1, 0] = -2
     assert not P.check_position_indices(i32(pos), continued=True)
+
+
+def test_cut_plan_rows_chained_on_gpu():
+    """A stream packed by the cut policy (rows filled to the end, sequences continued in
+    the next row), the rows run one after another on the GPU with the previous row's
+    final states: every output against the same chain on the oracle (fp32)."""
+    import torch
+    import oracle as O
+    import paper_2408_03865_amd as P
+    L, Dn = 1024, 32
+    ln = W.draw_stream_lengths(("lognormal", 6.0, 1.0, 16, 4096), np.random.default_rng(11), 12)
+    pieces, rows = P.pack_plan(ln, L, "cut")
+    pos = P.pack_positions(pieces, rows, L)
+    d = W.make_inputs(_cfg(rows, Dn, L, "f32"), variant="general")
+    d["pos"] = pos
+    g = {k: f32(d[k]) for k in (*W.ACTIVATIONS, "A", "D", "delta_bias", "w", "bias")}
+    sargs = lambda t, p: (t["u"], t["delta"], t["A"], t["B"], t["C"], t["D"], t["z"], t["delta_bias"], True, p)
+    xi = hi = None
+    oxi = ohi = None
+    for r in range(rows):
+        note(f"cut-plan row {r}")
+        t = {k: (v[r:r + 1].clone() if k in W.ACTIVATIONS else v) for k, v in g.items()}
+        p = i32(pos[r:r + 1])
+        c, xf = P.causal_conv1d_fwd(t["x"], t["w"], t["bias"], p, initial_x=xi, return_final=True)
+        y, hf = P.selective_scan_fwd(*sargs(t, p), initial_state=hi, return_final=True)
+        torch.cuda.synchronize()
+        od = {k: d[k][r:r + 1] for k in W.ACTIVATIONS}
+        oc, oxf = O.conv1d_fwd(od["x"], d["w"], d["bias"], pos[r:r + 1], xinit=oxi, return_final=True)
+        oy, ohf = O.scan_fwd(od["u"], od["delta"], d["A"], od["B"], od["C"], d["D"], od["z"], d["delta_bias"],
+                             True, pos[r:r + 1], h0=ohi, return_final=True)
+        assert_close(f"row {r} conv", host(c), oc, TOL["f32"])
+        assert_close(f"row {r} y", host(y), oy, TOL["f32"])
+        assert_close(f"row {r} final state", host(hf), ohf, TOL["f32"])
+        assert np.array_equal(host(xf), oxf)
+        xi, hi, oxi, ohi = xf, hf, oxf, ohf

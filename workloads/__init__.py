@@ -26,7 +26,7 @@ import numpy as np
 
 __all__ = [
     "Config", "CONFIGS", "config", "draw_row_lengths", "positions_from_lengths",
-    "make_inputs", "bf16_bits", "bf16_round", "pack", "unpack", "ACTIVATIONS",
+    "make_inputs", "bf16_bits", "bf16_round", "pack", "unpack", "ACTIVATIONS", "draw_stream_lengths",
 ]
 
 # Tensors stored in the path dtype (bf16 or fp32); everything else is fp32.
@@ -99,6 +99,15 @@ def _edge_starts(seqlen: int) -> List[int]:
         s.update(range(run0, run0 + 7))
     s.add(seqlen - 1)
     return sorted(x for x in s if 0 <= x < seqlen)
+
+
+def draw_stream_lengths(law: tuple, rng: np.random.Generator, count: int) -> np.ndarray:
+    """``count`` sequence lengths of a stream (int64), drawn as the log-normal law of
+    the workloads draws them, before any packing."""
+    if law[0] != "lognormal":
+        raise ValueError("stream lengths are drawn from a log-normal law")
+    mu, sigma, lo, hi = law[1:]
+    return np.clip(np.rint(np.exp(rng.normal(mu, sigma, size=count))), lo, hi).astype(np.int64)
 
 
 def draw_row_lengths(law: tuple, rng: np.random.Generator, batch: int, seqlen: int) -> List[List[int]]:
