@@ -275,6 +275,108 @@ def comparison(lib, tens, pos_host, code, width, stream, steps, warmup, packed_m
     return res
 
 
+BLOCK_PHASES = {"norm": "other", "in_proj": "gemm", "conv": "conv", "x_proj": "gemm", "scan": "scan",
+                "out_proj": "gemm", "out_proj_bwd": "gemm", "scan_bwd": "scan", "x_proj_bwd": "gemm",
+                "conv_bwd": "conv", "in_proj_bwd": "gemm", "norm_bwd": "other"}
+
+
+def block_bench(args):
+    """One packed Mamba-1 block (Mamba-1.4B layer: d_model 2048, d_inner 4096, d_state 16,
+    dt_rank 128, conv width 4, bf16), forward and backward, on the tokens of the 1.4B
+    workload: packed, padded to the longest sequence, and one sequence per call.  The
+    time per phase comes from events between the phases of each step."""
+    import numpy as np
+    import torch
+    import workloads as W
+    import paper_2408_03865_amd.block as BK
+
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    cfg = W.config("2")
+    Nb, L, Dn, N = cfg.batch, cfg.seqlen, cfg.dim, cfg.dstate
+    dm, R, Wd = 2048, 128, cfg.width
+    d = W.make_inputs(cfg)
+    g = torch.Generator(device=dev).manual_seed(0)
+    bf = torch.bfloat16
+    rn = lambda *sh: torch.randn(sh, generator=g, device=dev)  # noqa: E731
+    p = {"norm_w": torch.ones(dm, device=dev), "W_in": (rn(2 * Dn, dm) / dm ** 0.5).to(bf),
+         "conv_w": torch.from_numpy(d["w"]).to(dev), "conv_b": torch.zeros(Dn, device=dev),
+         "W_x": (rn(R + 2 * N, Dn) / Dn ** 0.5).to(bf), "W_dt": (rn(Dn, R) / R ** 0.5).to(bf),
+         "dt_bias": torch.from_numpy(d["delta_bias"]).to(dev), "A": torch.from_numpy(d["A"]).to(dev),
+         "D": torch.ones(Dn, device=dev), "W_out": (rn(dm, Dn) / Dn ** 0.5).to(bf)}
+    x = rn(Nb, dm, L).to(bf)
+    dout = rn(Nb, dm, L).to(bf)
+    pos = torch.from_numpy(d["pos"]).to(dev)
+
+    def run(xx, dd, pp, marks=None):
+        mk = None
+        if marks is not None:
+            def mk(name):
+                e = torch.cuda.Event(enable_timing=True)
+                e.record(stream)
+                marks.append((name, e))
+        out, ctx = BK.block_forward(xx, pp, p, mark=mk)
+        BK.block_backward(dd, ctx, p, mark=mk)
+
+    steps, warmup = args.steps, args.warmup
+    ms = time_steps(lambda: run(x, dout, pos), stream, steps, warmup)
+    # per-phase times, averaged over the steps
+    phase = {k: 0.0 for k in BLOCK_PHASES}
+    for _ in range(steps):
+        marks = []
+        run(x, dout, pos, marks)
+        torch.cuda.synchronize()
+        for (a, e0), (_, e1) in zip(marks, marks[1:]):
+            if a in phase:
+                phase[a] += e0.elapsed_time(e1) / steps
+    cat = {}
+    for k, v in phase.items():
+        cat[BLOCK_PHASES[k]] = cat.get(BLOCK_PHASES[k], 0.0) + v
+    tokens = Nb * L
+    res = {"metric": "packed Mamba-1.4B block fwd+bwd tokens/s", "value": round(tokens / (ms * 1e-3), 1),
+           "unit": "tokens/s", "ms_per_step": round(ms, 4), "steps": steps, "warmup": warmup,
+           "dtype": "bf16", "data": "synthetic",
+           "config": {"workload": "one Mamba-1.4B block: 8 packed rows x 4096 tokens, d_model 2048, d_inner 4096, "
+                                  "d_state 16, dt_rank 128, conv width 4, bf16 activations and projection weights",
+                      "batch": Nb, "seqlen": L},
+           "phase_ms": {k: round(v, 4) for k, v in phase.items()},
+           "class_ms": {k: round(v, 4) for k, v in cat.items()}}
+    # same tokens, padded and single
+    seqs = sequences(d["pos"])
+    lmax = max(n for _, _, n in seqs)
+    xp = torch.zeros((len(seqs), dm, lmax), dtype=bf, device=dev)
+    dp = torch.zeros_like(xp)
+    for i, (b, o, n) in enumerate(seqs):
+        xp[i, :, :n] = x[b, :, o:o + n]
+        dp[i, :, :n] = dout[b, :, o:o + n]
+    pp = torch.arange(lmax, dtype=torch.int32, device=dev).repeat(len(seqs), 1).contiguous()
+    msp = time_steps(lambda: run(xp, dp, pp), stream, 3, 1)
+    phase_p = {k: 0.0 for k in BLOCK_PHASES}
+    marks = []
+    run(xp, dp, pp, marks)
+    torch.cuda.synchronize()
+    for (a, e0), (_, e1) in zip(marks, marks[1:]):
+        if a in phase_p:
+            phase_p[a] += e0.elapsed_time(e1)
+    cat_p = {}
+    for k, v in phase_p.items():
+        cat_p[BLOCK_PHASES[k]] = cat_p.get(BLOCK_PHASES[k], 0.0) + v
+    del xp, dp
+    torch.cuda.empty_cache()
+    singles = [(x[b:b + 1, :, o:o + n].contiguous(), dout[b:b + 1, :, o:o + n].contiguous(),
+                torch.arange(n, dtype=torch.int32, device=dev)[None].contiguous()) for b, o, n in seqs]
+    mss = time_steps(lambda: [run(a, b_, c) for a, b_, c in singles], stream, 3, 1)
+    res["comparison"] = {
+        "padded": {"rows": len(seqs), "seqlen": lmax, "ms_per_step": round(msp, 4),
+                   "packed_speedup": round(msp / ms, 3),
+                   "class_ms": {k: round(v, 4) for k, v in cat_p.items()},
+                   "class_speedup": {k: round(cat_p[k] / cat[k], 3) for k in cat}},
+        "single": {"calls_per_step": len(seqs), "ms_per_step": round(mss, 4),
+                   "packed_speedup": round(mss / ms, 3)},
+    }
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -285,6 +387,9 @@ def main():
     ap.add_argument("--dtype", default=None, choices=["f32", "bf16"],
                     help="storage type of the activations, overriding the workload's (bf16 at the large shapes)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--block", action="store_true",
+                    help="time one packed Mamba-1.4B block (projections, norm, conv, scan), fwd+bwd, "
+                         "against padding and single-sequence calls, instead of the operator step")
     ap.add_argument("--no-compare", action="store_true",
                     help="skip the padded / single-sequence runs of the same tokens (Mamba-1.4B shape only)")
     ap.add_argument("--cpu-rows", type=int, default=8)
@@ -313,6 +418,12 @@ def main():
     import workloads as W
     from paper_2408_03865_amd import _lib
 
+    if args.block:
+        if not os.path.exists(_lib.LIB_PATH):
+            import __graft_entry__
+            __graft_entry__.build()
+        block_bench(args)
+        return
     if not os.path.exists(_lib.LIB_PATH):
         import __graft_entry__
         __graft_entry__.build()

@@ -1,0 +1,134 @@
+"""A packed Mamba-1 block on one GPU (§3.2): RMSNorm, input projection, packed causal
+conv1d + SiLU, x and dt projections, packed selective scan with the D skip and the
+SiLU(z) gate, output projection, residual -- forward and backward.
+
+The sequence-wise steps (conv, scan) run in this library's HIP kernels through the C
+ABI; the projections are plain GEMMs, run by hipBLASLt through torch.matmul; RMSNorm
+and the residual are token-wise torch operations (§3.2: token-wise and element-wise
+operators satisfy PUI unchanged, so packing needs nothing from them).  Activations are
+laid out (batch, features, seqlen), sequence innermost, which is the layout of the
+conv and scan kernels, so no transposes sit between the steps: each projection is a
+batched GEMM W @ X[b], split per output part so that every tensor the kernels see is
+contiguous.
+
+Parameters (dict of tensors on the device): norm_w (d_model), W_in (2*d_inner,
+d_model), conv_w (d_inner, W), conv_b (d_inner), W_x (R + 2N, d_inner), W_dt (d_inner,
+R), dt_bias (d_inner), A (d_inner, N), D (d_inner), W_out (d_model, d_inner).  The
+projection weights are in the activation dtype; the others are fp32.
+"""
+from __future__ import annotations
+
+from typing import Callable, Dict, Optional
+
+import paper_2408_03865_amd as P
+
+EPS = 1e-5
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _lin(W, X):
+    """Y[b] = W @ X[b]; X (batch, in, L) contiguous."""
+    return _torch().matmul(W, X)
+
+
+def _lin_dx(W, dY):
+    """dX[b] = W^T @ dY[b]."""
+    return _torch().matmul(W.t().contiguous(), dY)
+
+
+def _tokens_major(X):
+    """(batch, f, L) -> (batch*L, f), contiguous: the right operand of a weight gradient."""
+    return X.transpose(1, 2).reshape(-1, X.shape[1])
+
+
+def _lin_dw(dY, Xt):
+    """dW = sum_b dY[b] @ X[b]^T, with Xt = _tokens_major(X)."""
+    torch = _torch()
+    dY2 = dY.transpose(0, 1).reshape(dY.shape[1], -1)          # (out, batch*L)
+    return torch.matmul(dY2, Xt)
+
+
+def rmsnorm(x, w, eps=EPS):
+    torch = _torch()
+    xf = x.float()
+    r = torch.rsqrt(xf.pow(2).mean(1, keepdim=True) + eps)
+    return (xf * r * w[None, :, None]).to(x.dtype), r
+
+
+def rmsnorm_bwd(x, w, r, dh):
+    xh = x.float() * r
+    dhf = dh.float()
+    dw = (dhf * xh).sum((0, 2))
+    dxh = dhf * w[None, :, None]
+    dx = r * (dxh - xh * (dxh * xh).mean(1, keepdim=True))
+    return dx, dw
+
+
+def block_forward(x, pos, p: Dict[str, object], mark: Optional[Callable[[str], None]] = None):
+    """out = x + W_out @ scan(conv(W_in,x @ RMSNorm(x)), ...): returns (out, ctx)."""
+    mk = mark or (lambda name: None)
+    Dn = p["D"].shape[0]
+    N = p["A"].shape[1]
+    R = p["W_dt"].shape[1]
+    mk("norm")
+    h, r = rmsnorm(x, p["norm_w"])
+    mk("in_proj")
+    xi = _lin(p["W_in"][:Dn], h)
+    z = _lin(p["W_in"][Dn:], h)
+    mk("conv")
+    u = P.causal_conv1d_fwd(xi, p["conv_w"], p["conv_b"], pos, silu=True)
+    mk("x_proj")
+    Wx = p["W_x"]
+    dtl = _lin(Wx[:R], u)
+    B = _lin(Wx[R:R + N], u)
+    C = _lin(Wx[R + N:], u)
+    delta = _lin(p["W_dt"], dtl)
+    mk("scan")
+    y, st = P.selective_scan_fwd(u, delta, p["A"], B, C, p["D"], z, p["dt_bias"], True, pos,
+                                 return_states=True)
+    mk("out_proj")
+    out = x + _lin(p["W_out"], y)
+    mk("end")
+    ctx = dict(x=x, pos=pos, h=h, r=r, xi=xi, z=z, u=u, dtl=dtl, B=B, C=C, delta=delta, y=y, st=st)
+    return out, ctx
+
+
+def block_backward(dout, ctx, p, mark: Optional[Callable[[str], None]] = None) -> Dict[str, object]:
+    """Gradients of sum(dout * out) with respect to x and every parameter."""
+    mk = mark or (lambda name: None)
+    Dn = p["D"].shape[0]
+    N = p["A"].shape[1]
+    R = p["W_dt"].shape[1]
+    Wx = p["W_x"]
+    dt = dout.dtype
+    g = {}
+    mk("out_proj_bwd")
+    g["W_out"] = _lin_dw(dout, _tokens_major(ctx["y"]))
+    dy = _lin_dx(p["W_out"], dout)
+    mk("scan_bwd")
+    s = P.selective_scan_bwd(ctx["u"], ctx["delta"], p["A"], ctx["B"], ctx["C"], p["D"], ctx["z"],
+                             p["dt_bias"], True, ctx["pos"], dy, saved_states=ctx["st"])
+    g["A"], g["D"], g["dt_bias"] = s["dA"], s["dD"], s["ddelta_bias"]
+    mk("x_proj_bwd")
+    g["W_dt"] = _lin_dw(s["ddelta"], _tokens_major(ctx["dtl"]))
+    ddtl = _lin_dx(p["W_dt"], s["ddelta"])
+    dB, dC = s["dB"].to(dt), s["dC"].to(dt)
+    ut = _tokens_major(ctx["u"])
+    g["W_x"] = _torch().cat([_lin_dw(ddtl, ut), _lin_dw(dB, ut), _lin_dw(dC, ut)], 0)
+    du = s["du"] + _lin_dx(Wx[:R], ddtl) + _lin_dx(Wx[R:R + N], dB) + _lin_dx(Wx[R + N:], dC)
+    mk("conv_bwd")
+    dxi, g["conv_w"], g["conv_b"] = P.causal_conv1d_bwd(ctx["xi"], p["conv_w"], p["conv_b"], ctx["pos"],
+                                                        du.contiguous(), silu=True)
+    mk("in_proj_bwd")
+    ht = _tokens_major(ctx["h"])
+    g["W_in"] = _torch().cat([_lin_dw(dxi, ht), _lin_dw(s["dz"], ht)], 0)
+    dh = _lin_dx(p["W_in"][:Dn], dxi) + _lin_dx(p["W_in"][Dn:], s["dz"])
+    mk("norm_bwd")
+    dxn, g["norm_w"] = rmsnorm_bwd(ctx["x"], p["norm_w"], ctx["r"], dh)
+    g["x"] = (dout.float() + dxn).to(dt)
+    mk("end")
+    return g
