@@ -89,6 +89,28 @@ __device__ __forceinline__ void load_run(const T* __restrict__ row, int64_t l0, 
     }
 }
 
+// K consecutive elements at row[l0] as raw 16-byte vectors (l0 + K <= L, vector
+// aligned), converted later by unpack_run: the loads can be issued well before the
+// values are needed, e.g. ahead of a barrier.
+template <typename T, int K>
+struct RawRun {
+    u32x4 w[K / Storage<T>::kPerVec];
+};
+template <typename T, int K>
+__device__ __forceinline__ RawRun<T, K> load_raw(const T* __restrict__ row, int64_t l0) {
+    constexpr int PV = Storage<T>::kPerVec;
+    RawRun<T, K> r;
+#pragma unroll
+    for (int i = 0; i < K / PV; ++i) r.w[i] = *reinterpret_cast<const u32x4*>(row + l0 + i * PV);
+    return r;
+}
+template <typename T, int K>
+__device__ __forceinline__ void unpack_run(const RawRun<T, K>& r, float* v) {
+    constexpr int PV = Storage<T>::kPerVec;
+#pragma unroll
+    for (int i = 0; i < K / PV; ++i) Storage<T>::unpack(r.w[i], v + i * PV);
+}
+
 // Store K consecutive elements (rounding to T) at row[l0]; elements beyond L are dropped.
 template <typename T, int K, bool FULL = false>
 __device__ __forceinline__ void store_run(T* __restrict__ row, int64_t l0, int64_t L, bool vec,

@@ -39,10 +39,11 @@ constexpr int kWaves = kThreads / 64;
 constexpr int kSeg = kK + 4;        // padded lane segment: conflict-free 16-byte LDS reads
 
 struct __attribute__((aligned(16))) BwdSmem {
+    float red[2][kWaves][2][kCH];   // [state parity][wave][dB|dC][token]: per-wave channel sums
+                                    // (first: its addresses need no constant offset)
     float B[kN][16][kSeg];          // [state][lane][token]
     float C[kN][16][kSeg];
     float M[16][kSeg];              // 0, or -inf on a sequence start
-    float red[2][kWaves][2][kCH];   // [state parity][wave][dB|dC][token]: per-wave channel sums
     float A2[kRows][kN];            // A * log2(e)
     float xc[kRows][kN];            // dh at the first token of the chunk to the right
     float an[kRows][kN];            // Abar at the first token of the chunk to the right
@@ -158,6 +159,16 @@ void scan_bwd_kernel(BwdParams p) {
     auto chunk = [&](auto full_tag, const int64_t c) {
         constexpr bool FULL = decltype(full_tag)::value;
         const int64_t lb = c * kCH;
+        const int64_t l0 = lb + (int64_t)j * K;
+        // this lane's inputs, loaded first in a full chunk so that their latency
+        // overlaps the staging below
+        RawRun<T, K> wu, wd, wg, wz;
+        if constexpr (FULL) {
+            wu = load_raw<T, K>(ur, l0);
+            wd = load_raw<T, K>(dr, l0);
+            wg = load_raw<T, K>(gr, l0);
+            if (zr) wz = load_raw<T, K>(zr, l0);
+        }
         // ---- stage B, C, the reset mask and the chunk-start states in LDS ----
         for (int idx = tid * PV; idx < kN * kCH; idx += kThreads * PV) {
             const int n = idx / kCH, t = idx - n * kCH;
@@ -182,17 +193,23 @@ void scan_bwd_kernel(BwdParams p) {
         __syncthreads();
 
         // ---- per-token inputs ----
-        const int64_t l0 = lb + (int64_t)j * K;
         float dt[K], dlu[K], dyD[K], yacc[K], sdhB[K], sdA[K];
         float S = 0.0f, Mf = 0.0f, Mr = 0.0f, m0 = 0.0f;
         {
             float dl[K], uv[K];
-            load_run<T, K, FULL>(ur, l0, L, p.vec, uv);
-            load_run<T, K, FULL>(dr, l0, L, p.vec, dl);
-            load_run<T, K, FULL>(gr, l0, L, p.vec, dyD);     // dout for now
+            if constexpr (FULL) {
+                unpack_run(wu, uv);
+                unpack_run(wd, dl);
+                unpack_run(wg, dyD);                          // dout for now
+            } else {
+                load_run<T, K, FULL>(ur, l0, L, p.vec, uv);
+                load_run<T, K, FULL>(dr, l0, L, p.vec, dl);
+                load_run<T, K, FULL>(gr, l0, L, p.vec, dyD);
+            }
             if (zr) {
                 float zv[K], gz[K];
-                load_run<T, K, FULL>(zr, l0, L, p.vec, zv);
+                if constexpr (FULL) unpack_run(wz, zv);
+                else load_run<T, K, FULL>(zr, l0, L, p.vec, zv);
 #pragma unroll
                 for (int k = 0; k < K; ++k) {
                     const float sz = sigmoid_f(zv[k]);
@@ -238,6 +255,15 @@ void scan_bwd_kernel(BwdParams p) {
         dt_next = dpp<kNewBcast0>(0.0f, dt[0]);
         m_next = dpp<kNewBcast0>(0.0f, m0);
 
+        // per-thread LDS addresses of the dB/dC sums and the offset of this thread's
+        // partial (token red_t of dB or dC) inside the block's state-0 partials
+        const int wr = r & 3;                        // row inside the wave
+        float* const red_w = &sm.red[0][tid >> 6][wr >> 1][j * K + (K / 2) * (wr & 1)];
+        const int red_which = __builtin_amdgcn_readfirstlane(tid >> 7);   // 0: dB, 1: dC (per wave)
+        const int red_t = tid & (kCH - 1);
+        const float* const red_r = &sm.red[0][0][red_which][red_t];
+        float* const part_n = p.part_bc + ((b * p.groups + g) * 2 + red_which) * kN * L;
+        const uint32_t part_off = (uint32_t)(lb + red_t);
 #pragma unroll 1
         for (int n = 0; n < kN; ++n) {
             const float A2n = sm.A2[r][n];
@@ -333,21 +359,14 @@ void scan_bwd_kernel(BwdParams p) {
                                                                  __float_as_uint(R[k + K / 2]), false, false);
                 Q[k] = __uint_as_float(s2[0]) + __uint_as_float(s2[1]);
             }
-            {
-                const int wr = r & 3;                // row inside the wave
-                *reinterpret_cast<f32x4*>(&sm.red[n & 1][tid >> 6][wr >> 1][j * K + (K / 2) * (wr & 1)]) =
-                    f32x4{Q[0], Q[1], Q[2], Q[3]};
-            }
+            const int par = (n & 1) * (kWaves * 2 * kCH);
+            *reinterpret_cast<f32x4*>(red_w + par) = f32x4{Q[0], Q[1], Q[2], Q[3]};
             __syncthreads();
             {   // then over the block's 4 waves, in a fixed order
-                const int which = tid >> 7;          // 0: dB, 1: dC
-                const int t = tid & (kCH - 1);
                 float s = 0.0f;
 #pragma unroll
-                for (int q = 0; q < kWaves; ++q) s += sm.red[n & 1][q][which][t];
-                const int64_t l = lb + t;
-                if (FULL || l < L)
-                    p.part_bc[(((b * p.groups + g) * 2 + which) * kN + n) * L + l] = s;
+                for (int q = 0; q < kWaves; ++q) s += red_r[par + q * 2 * kCH];
+                if (FULL || lb + red_t < L) part_n[n * L + part_off] = s;
             }
             // no second barrier: the next state writes the other buffer, and this one is
             // rewritten only after every thread has passed the next state's barrier

@@ -119,6 +119,14 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_kernel(FwdParams p) {
     auto chunk = [&](auto full_tag, const int64_t c) {
         constexpr bool FULL = decltype(full_tag)::value;
         const int64_t lb = c * CH;
+        const int64_t l0 = lb + (int64_t)j * K;
+        // this lane's inputs, loaded first in a full chunk so that their latency
+        // overlaps the staging below
+        RawRun<T, K> wu, wd;
+        if constexpr (FULL) {
+            wu = load_raw<T, K>(ur, l0);
+            wd = load_raw<T, K>(dr, l0);
+        }
         // ---- stage B, C and the reset mask of this chunk in LDS ----
         for (int idx = tid * PV; idx < kN * CH; idx += kThreads * PV) {
             const int n = idx / CH, t = idx - n * CH;
@@ -140,12 +148,16 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_kernel(FwdParams p) {
         __syncthreads();
 
         // ---- per-token inputs of this lane ----
-        const int64_t l0 = lb + (int64_t)j * K;
         float dt[K], du[K], y[K], M[K];
         {
             float uv[K];
-            load_run<T, K, FULL>(ur, l0, L, p.vec, uv);
-            load_run<T, K, FULL>(dr, l0, L, p.vec, dt);
+            if constexpr (FULL) {
+                unpack_run(wu, uv);
+                unpack_run(wd, dt);
+            } else {
+                load_run<T, K, FULL>(ur, l0, L, p.vec, uv);
+                load_run<T, K, FULL>(dr, l0, L, p.vec, dt);
+            }
 #pragma unroll
             for (int k = 0; k < K; ++k) {
                 const float s = dt[k] + dbias;
