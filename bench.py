@@ -183,6 +183,26 @@ def time_steps(step_fn, stream, steps, warmup):
     return e0.elapsed_time(e1) / steps
 
 
+def cold_steps(step_fn, stream, steps, flush_bytes=1 << 29):
+    """Median time of one step with the caches cold: before each step (outside its
+    events) a fill of ``flush_bytes`` evicts the L2s and the 256 MB memory-side cache,
+    so the step's inputs come from HBM even where the previous step left them cached."""
+    import numpy as np
+    import torch
+    buf = torch.empty(flush_bytes // 4, dtype=torch.float32, device=stream.device)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for it, (e0, e1) in enumerate(evs):
+        buf.fill_(float(it))
+        e0.record(stream)
+        step_fn()
+        e1.record(stream)
+    torch.cuda.synchronize()
+    ms = [e0.elapsed_time(e1) for e0, e1 in evs]
+    del buf
+    return {"ms_per_step": round(float(np.median(ms)), 4), "flush_bytes": int(flush_bytes),
+            "steps": steps}
+
+
 def with_states(lib, tens, pos_host, code, width, stream, steps, warmup, packed_ms):
     """The same step with every row continuing a sequence cut at the end of another row
     (its first sequence's position indices start at 100), initial states in, final
@@ -482,8 +502,10 @@ def main():
             f()
             evs[it][i + 1].record(stream)
     torch.cuda.synchronize()
-    op_ms = {name: float(np.mean([evs[it][i].elapsed_time(evs[it][i + 1]) for it in range(args.steps)]))
+    op_ms = {name: float(np.median([evs[it][i].elapsed_time(evs[it][i + 1]) for it in range(args.steps)]))
              for i, (name, _) in enumerate(ops)}
+    cold = cold_steps(step, stream, args.steps)
+    cold["tokens_per_s"] = round(Nb * L / (cold["ms_per_step"] * 1e-3), 1)
 
     mb = minimal_bytes(Nb, Dn, L, N, Wd, s)
     total_bytes = sum(mb.values())
@@ -521,6 +543,7 @@ def main():
         "scan_hbm_frac": round((mb["scan_fwd"] + mb["scan_bwd"]) /
                                ((op_ms["scan_fwd"] + op_ms["scan_bwd"]) * 1e-3) / HBM_PEAK, 4),
         "roofline": roof,
+        "cold_cache": cold,
         "device": torch.cuda.get_device_name(0),
     }
     if args.config == "2" and not args.no_compare:

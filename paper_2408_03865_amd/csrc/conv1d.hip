@@ -19,11 +19,12 @@ constexpr int kTok = 8;        // tokens per thread per step (forward), and the 
 constexpr int kTokBwd = 8;     // tokens per thread per step (backward)
 constexpr int kThreads = 256;
 
-// N position indices from l0 (N a multiple of 4); beyond L they read 0
-template <int N = kTok>
+// N position indices from l0 (N a multiple of 4); beyond L they read 0.  FULL: the
+// caller guarantees l0 + N <= L and 16-byte alignment
+template <int N = kTok, bool FULL = false>
 __device__ __forceinline__ void load_pos(const int32_t* __restrict__ pr, int64_t l0, int64_t L,
                                          bool pvec, int* p) {
-    if (pvec && l0 + N <= L) {
+    if (FULL || (pvec && l0 + N <= L)) {
 #pragma unroll
         for (int i = 0; i < N; i += 4) {
             const u32x4 a = *reinterpret_cast<const u32x4*>(pr + l0 + i);
@@ -61,9 +62,9 @@ __device__ __forceinline__ void load_row_halo(const T* __restrict__ xinit, int64
 // l0 + t and xs[kTok - 1 - t] holds token l0 - 1 - t
 template <int W>
 __device__ __forceinline__ float conv_pre(const float* xs, int i, int p, const float* wk, float b0) {
-    float acc = b0;
+    float acc = fmaf(wk[W - 1], xs[kTok + i], b0);      // tap 0: position indices are >= 0
 #pragma unroll
-    for (int k = 0; k < W; ++k)
+    for (int k = 1; k < W; ++k)
         if (k <= p) acc = fmaf(wk[W - 1 - k], xs[kTok + i - k], acc);
     return acc;
 }
@@ -135,19 +136,24 @@ __device__ __forceinline__ void block_sum(float* v, float* lds /* NV * (kThreads
     }
 }
 
-// Backward: each thread owns KT consecutive tokens per step and also recomputes
-// the activation gradient of the next W-1 tokens (the reverse-index halo).  DXF:
-// a final-input gradient is given (a separate instantiation, so that the common
-// path keeps its register count).
+// Backward: one wave per row, walking it from the end in steps of 64*KT tokens.
+// Each lane owns KT consecutive tokens per step and computes their activation
+// gradient g once.  dx of a token needs g of the next W-1 tokens (the reverse-index
+// halo): they belong to the next lane, which hands over their masked values with a
+// lane shift, and for lane 63 to lane 0 of the previous (later) step, whose values
+// are carried.
+// DXF: a final-input gradient is given (a separate instantiation, so that the
+// common path keeps its register count).
 template <typename T, typename TO, int W, int KT, bool DXF>
-__global__ __launch_bounds__(kThreads) void conv1d_bwd_kernel(
+__global__ __launch_bounds__(64) void conv1d_bwd_kernel(
     const T* __restrict__ x, const float* __restrict__ w, const float* __restrict__ bias,
     const int32_t* __restrict__ pos, const T* __restrict__ dout, TO* __restrict__ dx,
     float* __restrict__ partial, ConvStates<T, TO> st, int64_t dim, int64_t L, int silu, int vec,
     int pvec) {
-    __shared__ float red[(W + 1) * (kThreads / 64)];
+    static_assert(KT >= W - 1 && KT % 4 == 0, "the halo lies in the next lane's tokens");
     const int64_t row = blockIdx.x;
     const int64_t b = row / dim, d = row - b * dim;
+    const int lane = (int)threadIdx.x;
     const T* xr = x + row * L;
     const T* gr = dout + row * L;
     TO* dxr = dx + row * L;
@@ -159,35 +165,64 @@ __global__ __launch_bounds__(kThreads) void conv1d_bwd_kernel(
     float acc[W + 1];   // dw[0..W-1], dbias
 #pragma unroll
     for (int j = 0; j <= W; ++j) acc[j] = 0.0f;
+    // masked activation gradients gm[k][t] (k > t, t < W-1) of the first W-1 tokens of
+    // lane 0 in the step to the right (past the row end: 0)
+    float cgm[W][W - 1];
+#pragma unroll
+    for (int k = 0; k < W; ++k) {
+#pragma unroll
+        for (int t = 0; t < W - 1; ++t) cgm[k][t] = 0.0f;
+    }
 
-    for (int64_t l0 = (int64_t)threadIdx.x * KT; l0 < L; l0 += (int64_t)kThreads * KT) {
-        // x for tokens l0-8 .. l0+KT+7 (pre-activations of this run and the next W-1 tokens)
-        float xs[kTok + KT + kTok];
-        if (l0 > 0) load_run<T, kTok>(xr, l0 - kTok, L, vec, xs);
+    constexpr int64_t kSpan = 64 * KT;
+    const int64_t nsteps = (L + kSpan - 1) / kSpan;
+    // One step; FULL (wave-uniform) means the step lies inside the row and vector access
+    // is allowed, so the loads and stores need no bounds checks.
+    auto step = [&](auto full_tag, const int64_t sidx) {
+        constexpr bool FULL = decltype(full_tag)::value;
+        const int64_t l0 = sidx * kSpan + (int64_t)lane * KT;
+        // x of tokens l0-8 .. l0+KT-1 (pre-activations of this lane's tokens)
+        float xs[kTok + KT];
+        if (l0 > 0) load_run<T, kTok, FULL>(xr, l0 - kTok, L, vec, xs);
         else load_row_halo<T, W>(st.xinit, row, xs);
-        load_run<T, KT>(xr, l0, L, vec, xs + kTok);
-        load_run<T, kTok>(xr, l0 + KT, L, vec, xs + kTok + KT);
-        float gs[KT + kTok];
-        load_run<T, KT>(gr, l0, L, vec, gs);
-        load_run<T, kTok>(gr, l0 + KT, L, vec, gs + KT);
-        int p[KT + kTok];
-        load_pos<KT>(pr, l0, L, pvec, p);
-        load_pos<kTok>(pr, l0 + KT, L, pvec, p + KT);
-        // gm[k][t] = g[t] if tap k of token t is live (k <= pos[t]) else 0, for tokens
-        // l0 .. l0+KT+W-2, g = dout * d out / d pre (0 beyond L: dout reads 0).  The
-        // same masked values give dx through the reverse indices (tap k of token j
-        // is live iff pos[j+k] >= k) and dw.
+        load_run<T, KT, FULL>(xr, l0, L, vec, xs + kTok);
+        float gs[KT];
+        load_run<T, KT, FULL>(gr, l0, L, vec, gs);   // 0 beyond L, so g = 0 there
+        int p[KT];
+        load_pos<KT, FULL>(pr, l0, L, pvec, p);
+        // gm[k][t] = g[t] if tap k of token t is live (k <= pos[t]) else 0, with g the
+        // activation gradient.  The same masked values give dx through the reverse
+        // indices (tap k of token j is live iff pos[j+k] >= k) and dw.  Tap 0 is always
+        // live (position indices are >= 0).
         float gm[W][KT + W - 1];
 #pragma unroll
-        for (int t = 0; t < KT + W - 1; ++t) {
+        for (int t = 0; t < KT; ++t) {
+            bool live[W];
+#pragma unroll
+            for (int k = 1; k < W; ++k) live[k] = k <= p[t];
             float gt = gs[t];
             if (silu) {
-                const float v = conv_pre<W>(xs, t, p[t], wk, b0);
-                const float s = sigmoid_f(v);
-                gt *= s * (1.0f + v * (1.0f - s));
-            }
+                float v = fmaf(wk[W - 1], xs[kTok + t], b0);
 #pragma unroll
-            for (int k = 0; k < W; ++k) gm[k][t] = (k <= p[t]) ? gt : 0.0f;
+                for (int k = 1; k < W; ++k)
+                    if (live[k]) v = fmaf(wk[W - 1 - k], xs[kTok + t - k], v);
+                const float sg = sigmoid_f(v);
+                gt *= sg * (1.0f + v * (1.0f - sg));
+            }
+            gm[0][t] = gt;
+#pragma unroll
+            for (int k = 1; k < W; ++k) gm[k][t] = live[k] ? gt : 0.0f;
+        }
+        // the next W-1 tokens (only the taps that reach back into this lane): from the
+        // next lane, or for lane 63 from the carry; then lane 0's become the carry
+#pragma unroll
+        for (int t = 0; t < W - 1; ++t) {
+#pragma unroll
+            for (int k = t + 1; k < W; ++k) {
+                const float h = __shfl_down(gm[k][t], 1, 64);
+                gm[k][KT + t] = lane == 63 ? cgm[k][t] : h;
+                cgm[k][t] = __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, gm[k][t])));
+            }
         }
         float o[KT];
 #pragma unroll
@@ -205,48 +240,39 @@ __global__ __launch_bounds__(kThreads) void conv1d_bwd_kernel(
                 if (j >= 0 && l0 + i < L) o[i] += Storage<T>::load1(st.dxfinal + row * (W - 1) + j);
             }
         }
-        store_run<TO, KT>(dxr, l0, L, vec, o);
-        // parameter gradients from this thread's own tokens
+        store_run<TO, KT, FULL>(dxr, l0, L, vec, o);
+        // parameter gradients from this lane's own tokens
 #pragma unroll
         for (int i = 0; i < KT; ++i) {
 #pragma unroll
             for (int k = 0; k < W; ++k) acc[W - 1 - k] = fmaf(gm[k][i], xs[kTok + i - k], acc[W - 1 - k]);
             acc[W] += gm[0][i];
         }
+    };
+    for (int64_t sidx = nsteps - 1; sidx >= 0; --sidx) {
+        if (vec && pvec && (sidx + 1) * kSpan <= L) step(std::true_type{}, sidx);
+        else step(std::false_type{}, sidx);
     }
-    // gradient of the inputs before the row, by one thread: initial input j (token
-    // j-W+1) meets output token t <= j through tap k = t-j+W-1 (weight w[j-t]), live
-    // iff k <= pos[t]; the activation gradient of those W-1 tokens is recomputed
-    if (st.dxinit && threadIdx.x == 0) {
-        float xs[2 * kTok], gs[kTok];
-        int p[kTok];
-        load_row_halo<T, W>(st.xinit, row, xs);
-        load_run<T, kTok>(xr, 0, L, vec, xs + kTok);
-        load_run<T, kTok>(gr, 0, L, vec, gs);
-        load_pos(pr, 0, L, pvec, p);
-        float g[W - 1];
-#pragma unroll
-        for (int t = 0; t < W - 1; ++t) {
-            g[t] = gs[t];
-            if (silu) {
-                const float v = conv_pre<W>(xs, t, p[t], wk, b0);
-                const float sg = sigmoid_f(v);
-                g[t] *= sg * (1.0f + v * (1.0f - sg));
-            }
-        }
+    // gradient of the inputs before the row: initial input j (token j-W+1) meets output
+    // token t <= j through tap k = t-j+W-1 > t (weight w[j-t]); the carry now holds the
+    // masked gradients of tokens 0..W-2
+    if (st.dxinit && lane == 0) {
 #pragma unroll
         for (int j = 0; j < W - 1; ++j) {
             float a = 0.0f;
 #pragma unroll
-            for (int t = 0; t <= j; ++t)
-                if (t - j + W - 1 <= p[t]) a = fmaf(wk[j - t], g[t], a);
+            for (int t = 0; t <= j; ++t) a = fmaf(wk[j - t], cgm[t - j + W - 1][t], a);
             // a row shorter than W-1 copies initial input j >= L to final input j - L
             if (st.dxfinal && j >= L) a += Storage<T>::load1(st.dxfinal + row * (W - 1) + (j - L));
             Storage<TO>::store1(st.dxinit + row * (W - 1) + j, a);
         }
     }
-    block_sum<W + 1>(acc, red);
-    if (threadIdx.x == 0) {
+#pragma unroll
+    for (int j = 0; j <= W; ++j) {
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) acc[j] += __shfl_xor(acc[j], off, 64);
+    }
+    if (lane == 0) {
 #pragma unroll
         for (int j = 0; j <= W; ++j) partial[row * (W + 1) + j] = acc[j];
     }
@@ -286,7 +312,7 @@ void conv_bwd_w(const ConvArgs& a, hipStream_t s, int vec, int pvec) {
     const ConvStates<T, TO> st{static_cast<const T*>(a.xinit), nullptr, static_cast<const T*>(a.dxfinal),
                                static_cast<TO*>(a.dxinit)};
     hipLaunchKernelGGL((conv1d_bwd_kernel<T, TO, W, kTokBwd, DXF>), dim3((unsigned)(a.batch * a.dim)),
-                       dim3(kThreads), 0, s, static_cast<const T*>(a.x), a.w, a.bias, a.pos,
+                       dim3(64), 0, s, static_cast<const T*>(a.x), a.w, a.bias, a.pos,
                        static_cast<const T*>(a.dout), static_cast<TO*>(a.out), a.partial, st, a.dim,
                        a.seqlen, a.silu, vec, pvec);
 }
