@@ -122,7 +122,8 @@ int packmamba_causal_conv1d_fwd(const void* x, const float* weight, const float*
 size_t packmamba_causal_conv1d_bwd_workspace_size(int64_t batch, int64_t dim, int64_t seqlen,
                                                   int32_t width) {
     if (check_shape(batch, dim, seqlen) || width < 2 || width > 4) return 0;
-    return align_up(sizeof(float) * (size_t)(batch * dim * (width + 1)));
+    const int64_t nseg = pm::conv_bwd_segments(batch, dim, seqlen);
+    return align_up(sizeof(float) * (size_t)(batch * nseg * dim * (width + 1)));
 }
 
 int packmamba_causal_conv1d_bwd(const void* x, const float* weight, const float* bias,

@@ -136,7 +136,9 @@ __device__ __forceinline__ void block_sum(float* v, float* lds /* NV * (kThreads
     }
 }
 
-// Backward: one wave per row, walking it from the end in steps of 64*KT tokens.
+// Backward: one wave per (row, segment), walking the segment from its end in steps
+// of 64*KT tokens (long rows with few channels are cut into segments of whole steps,
+// so that the grid has enough waves).
 // Each lane owns KT consecutive tokens per step and computes their activation
 // gradient g once.  dx of a token needs g of the next W-1 tokens (the reverse-index
 // halo): they belong to the next lane, which hands over their masked values with a
@@ -153,6 +155,7 @@ __global__ __launch_bounds__(64) void conv1d_bwd_kernel(
     static_assert(KT >= W - 1 && KT % 4 == 0, "the halo lies in the next lane's tokens");
     const int64_t row = blockIdx.x;
     const int64_t b = row / dim, d = row - b * dim;
+    const int seg = blockIdx.y, nseg = gridDim.y;
     const int lane = (int)threadIdx.x;
     const T* xr = x + row * L;
     const T* gr = dout + row * L;
@@ -162,20 +165,44 @@ __global__ __launch_bounds__(64) void conv1d_bwd_kernel(
 #pragma unroll
     for (int k = 0; k < W; ++k) wk[k] = w[d * W + k];
     const float b0 = bias ? bias[d] : 0.0f;
+    constexpr int64_t kSpan = 64 * KT;
+    static_assert(kSpan == kConvBwdSpan, "segments hold whole steps");
+    const int64_t nsteps = (L + kSpan - 1) / kSpan;
+    const int64_t seg_steps = (nsteps + nseg - 1) / nseg;
+    const int64_t s0 = (int64_t)seg * seg_steps;
+    const int64_t s1 = min(nsteps, s0 + seg_steps);
     float acc[W + 1];   // dw[0..W-1], dbias
 #pragma unroll
     for (int j = 0; j <= W; ++j) acc[j] = 0.0f;
     // masked activation gradients gm[k][t] (k > t, t < W-1) of the first W-1 tokens of
-    // lane 0 in the step to the right (past the row end: 0)
+    // lane 0 in the step to the right: 0 past the row end; at the end of a segment that
+    // is not the row's last, recomputed here (the same value in every lane)
     float cgm[W][W - 1];
 #pragma unroll
     for (int k = 0; k < W; ++k) {
 #pragma unroll
         for (int t = 0; t < W - 1; ++t) cgm[k][t] = 0.0f;
     }
-
-    constexpr int64_t kSpan = 64 * KT;
-    const int64_t nsteps = (L + kSpan - 1) / kSpan;
+    if (s1 * kSpan < L) {
+        const int64_t e = s1 * kSpan;               // first token after the segment
+#pragma unroll
+        for (int t = 0; t < W - 1; ++t) {
+            const int64_t l = e + t;
+            if (l >= L) break;
+            const int p = pr[l];
+            float g = Storage<T>::load1(gr + l);
+            if (silu) {
+                float v = b0;
+#pragma unroll
+                for (int k = 0; k < W; ++k)
+                    if (k <= p) v = fmaf(wk[W - 1 - k], Storage<T>::load1(xr + l - k), v);
+                const float sg = sigmoid_f(v);
+                g *= sg * (1.0f + v * (1.0f - sg));
+            }
+#pragma unroll
+            for (int k = t + 1; k < W; ++k) cgm[k][t] = k <= p ? g : 0.0f;
+        }
+    }
     // One step; FULL (wave-uniform) means the step lies inside the row and vector access
     // is allowed, so the loads and stores need no bounds checks.
     auto step = [&](auto full_tag, const int64_t sidx) {
@@ -249,14 +276,14 @@ __global__ __launch_bounds__(64) void conv1d_bwd_kernel(
             acc[W] += gm[0][i];
         }
     };
-    for (int64_t sidx = nsteps - 1; sidx >= 0; --sidx) {
+    for (int64_t sidx = s1 - 1; sidx >= s0; --sidx) {
         if (vec && pvec && (sidx + 1) * kSpan <= L) step(std::true_type{}, sidx);
         else step(std::false_type{}, sidx);
     }
     // gradient of the inputs before the row: initial input j (token j-W+1) meets output
     // token t <= j through tap k = t-j+W-1 > t (weight w[j-t]); the carry now holds the
     // masked gradients of tokens 0..W-2
-    if (st.dxinit && lane == 0) {
+    if (st.dxinit && seg == 0 && lane == 0) {
 #pragma unroll
         for (int j = 0; j < W - 1; ++j) {
             float a = 0.0f;
@@ -273,12 +300,14 @@ __global__ __launch_bounds__(64) void conv1d_bwd_kernel(
         for (int off = 32; off >= 1; off >>= 1) acc[j] += __shfl_xor(acc[j], off, 64);
     }
     if (lane == 0) {
+        float* pp = partial + ((b * nseg + seg) * dim + d) * (W + 1);
 #pragma unroll
-        for (int j = 0; j <= W; ++j) partial[row * (W + 1) + j] = acc[j];
+        for (int j = 0; j <= W; ++j) pp[j] = acc[j];
     }
 }
 
-// dw[d,k] = sum_b partial[b,d,k]; dbias[d] = sum_b partial[b,d,W]  (fixed order over b)
+// dw[d,k] = sum_r partial[r,d,k]; dbias[d] = sum_r partial[r,d,W] over the (batch row,
+// segment) pairs r, in a fixed order
 __global__ void conv1d_bwd_finalize(const float* __restrict__ partial, float* __restrict__ dw,
                                     float* __restrict__ dbias, int64_t batch, int64_t dim, int W) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -311,7 +340,8 @@ template <typename T, typename TO, int W, bool DXF>
 void conv_bwd_w(const ConvArgs& a, hipStream_t s, int vec, int pvec) {
     const ConvStates<T, TO> st{static_cast<const T*>(a.xinit), nullptr, static_cast<const T*>(a.dxfinal),
                                static_cast<TO*>(a.dxinit)};
-    hipLaunchKernelGGL((conv1d_bwd_kernel<T, TO, W, kTokBwd, DXF>), dim3((unsigned)(a.batch * a.dim)),
+    const unsigned nseg = (unsigned)conv_bwd_segments(a.batch, a.dim, a.seqlen);
+    hipLaunchKernelGGL((conv1d_bwd_kernel<T, TO, W, kTokBwd, DXF>), dim3((unsigned)(a.batch * a.dim), nseg),
                        dim3(64), 0, s, static_cast<const T*>(a.x), a.w, a.bias, a.pos,
                        static_cast<const T*>(a.dout), static_cast<TO*>(a.out), a.partial, st, a.dim,
                        a.seqlen, a.silu, vec, pvec);
@@ -329,9 +359,11 @@ hipError_t conv_bwd_t(const ConvArgs& a, hipStream_t s) {
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
+    // the partials of every (batch row, segment) are summed like batch rows
     const int64_t n = a.dim * (a.width + 1);
     hipLaunchKernelGGL(conv1d_bwd_finalize, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,
-                       a.partial, a.dw, a.dbias, a.batch, a.dim, (int)a.width);
+                       a.partial, a.dw, a.dbias, a.batch * conv_bwd_segments(a.batch, a.dim, a.seqlen),
+                       a.dim, (int)a.width);
     return hipGetLastError();
 }
 

@@ -17,7 +17,7 @@ struct ConvArgs {
     void* out;          // fwd: out; bwd: dx
     float* dw;          // bwd only
     float* dbias;       // bwd only
-    float* partial;     // bwd only: (batch*dim, width+1)
+    float* partial;     // bwd only: (batch, segments, dim, width+1)
     // state passing across rows, each (batch, dim, width-1) or null
     const void* xinit;  // inputs before the row (x's dtype)
     void* xfinal;       // fwd: the row's last width-1 inputs (x's dtype)
@@ -29,6 +29,20 @@ struct ConvArgs {
 
 hipError_t launch_conv1d_fwd(const ConvArgs& a, hipStream_t s);
 hipError_t launch_conv1d_bwd(const ConvArgs& a, hipStream_t s);
+
+// The conv backward runs one wave per (row, segment); a row is cut into segments of
+// whole 512-token steps when batch x dim alone gives fewer than kConvBwdWaves waves.
+constexpr int64_t kConvBwdSpan = 512;
+constexpr int64_t kConvBwdWaves = 4096;
+inline int64_t conv_bwd_segments(int64_t batch, int64_t dim, int64_t seqlen) {
+    const int64_t steps = (seqlen + kConvBwdSpan - 1) / kConvBwdSpan;
+    const int64_t rows = batch * dim;
+    int64_t nseg = (kConvBwdWaves + rows - 1) / rows;
+    if (nseg > steps) nseg = steps;
+    if (nseg < 1) nseg = 1;
+    const int64_t per = (steps + nseg - 1) / nseg;       // steps per segment
+    return (steps + per - 1) / per;                     // no empty segment
+}
 
 struct ScanArgs {
     const void* u;
