@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define PACKMAMBA_ABI_VERSION 3
+#define PACKMAMBA_ABI_VERSION 4
 
 /* dtype codes of the activation tensors */
 #define PACKMAMBA_F32 0            /* fp32 inputs, fp32 outputs */
@@ -201,6 +201,35 @@ int packmamba_selective_scan_bwd(const void* u, const void* delta, const float* 
                                  void* workspace, size_t workspace_bytes,
                                  int64_t batch, int64_t dim, int64_t seqlen, int32_t dstate,
                                  int32_t dtype, void* stream);
+
+/*
+ * RMSNorm of the packed Mamba block (§3.2: a token-wise operator, which packing
+ * leaves unchanged; no position indices are involved).  Over the feature axis of
+ * x (batch, dim, seqlen), at every token:
+ *   rstd[b,l] = 1 / sqrt(mean_d x[b,d,l]^2 + eps),  out = x * rstd * weight[d].
+ *   weight (dim) float; rstd (batch, seqlen) float, written for the backward;
+ *   out has x's shape and the dtype's output type.  eps >= 0 (PACKMAMBA_ERR_SHAPE
+ *   otherwise).  Per-token sums use a fixed order.
+ */
+int packmamba_rmsnorm_fwd(const void* x, const float* weight, float eps, void* out, float* rstd,
+                          int64_t batch, int64_t dim, int64_t seqlen, int32_t dtype, void* stream);
+
+/* Bytes of workspace packmamba_rmsnorm_bwd needs. */
+size_t packmamba_rmsnorm_bwd_workspace_size(int64_t batch, int64_t dim, int64_t seqlen);
+
+/*
+ * RMSNorm backward: with g = dout and s = sum_d g * weight * x at each token,
+ *   dx = rstd * (g * weight - x * rstd^2 * s / dim) + dresidual,
+ *   dweight[d] = sum_{b,l} g * x * rstd.
+ *   x, dout, dresidual (NULL: none; the gradient reaching x through a residual
+ *   connection) in the input type; dx in the output type; rstd as written by the
+ *   forward; dweight (dim) float, overwritten.  The sum for dweight uses per-tile
+ *   partials in the workspace and a second pass in fixed order (reproducible).
+ */
+int packmamba_rmsnorm_bwd(const void* x, const float* weight, const float* rstd, const void* dout,
+                          const void* dresidual, void* dx, float* dweight, void* workspace,
+                          size_t workspace_bytes, int64_t batch, int64_t dim, int64_t seqlen,
+                          int32_t dtype, void* stream);
 
 /*
  * Checks the index contract of §3.1 on the device: stores 1 to *d_flag (a device

@@ -31,6 +31,7 @@ from ._lib import BF16, BF16_F32OUT, F32, STATE_STRIDE, PackMambaError, load
 __all__ = [
     "causal_conv1d_fwd", "causal_conv1d_bwd", "selective_scan_fwd", "selective_scan_bwd",
     "check_position_indices", "saved_states_size", "segments", "pack_plan", "pack_positions",
+    "rmsnorm_fwd", "rmsnorm_bwd",
     "padding_rate", "PackMambaError", "load", "F32", "BF16",
     "STATE_STRIDE", "BF16_F32OUT",
 ]
@@ -106,6 +107,34 @@ def causal_conv1d_bwd(x, weight, bias, position_indices, dout, silu: bool = True
                                          _stream(x))
     _lib.check("packmamba_causal_conv1d_bwd", st)
     return (dx, dw, db) if initial_x is None else (dx, dw, db, dinit)
+
+
+def rmsnorm_fwd(x, weight, eps: float = 1e-5, out_f32: bool = False):
+    """RMSNorm over the feature axis of x (batch, dim, seqlen): (out, rstd), rstd
+    (batch, seqlen) fp32 for the backward."""
+    torch = _torch()
+    Nb, Dn, L = x.shape
+    out = _empty_out(x, out_f32)
+    rstd = torch.empty((Nb, L), dtype=torch.float32, device=x.device)
+    st = load().packmamba_rmsnorm_fwd(_p(x), _p(weight), float(eps), _p(out), _p(rstd), Nb, Dn, L,
+                                      _code(x, out_f32), _stream(x))
+    _lib.check("packmamba_rmsnorm_fwd", st)
+    return out, rstd
+
+
+def rmsnorm_bwd(x, weight, rstd, dout, dresidual=None, workspace=None, out_f32: bool = False):
+    """(dx, dweight); dresidual, if given, is added to dx (a residual connection)."""
+    torch = _torch()
+    Nb, Dn, L = x.shape
+    lib = load()
+    dx = _empty_out(x, out_f32)
+    dw = torch.empty_like(weight)
+    need = lib.packmamba_rmsnorm_bwd_workspace_size(Nb, Dn, L)
+    ws = workspace if workspace is not None else _workspace(need, x.device)
+    st = lib.packmamba_rmsnorm_bwd(_p(x), _p(weight), _p(rstd), _p(dout), _p(dresidual), _p(dx), _p(dw),
+                                   _p(ws), ws.numel(), Nb, Dn, L, _code(x, out_f32), _stream(x))
+    _lib.check("packmamba_rmsnorm_bwd", st)
+    return dx, dw
 
 
 def segments(batch: int, dim: int, seqlen: int) -> int:

@@ -15,7 +15,7 @@ LIB_PATH = os.path.join(HERE, "libpackmamba.so")
 
 F32, BF16, BF16_F32OUT = 0, 1, 2
 STATE_STRIDE = 128
-ABI_VERSION = 3
+ABI_VERSION = 4
 
 STATUS = {0: "OK", 1: "ERR_NULL", 2: "ERR_SHAPE", 3: "ERR_UNSUPPORTED", 4: "ERR_ALIGN",
           5: "ERR_WORKSPACE", 6: "ERR_LAUNCH"}
@@ -28,6 +28,7 @@ EXPORTS = (
     "packmamba_selective_scan_fwd_workspace_size", "packmamba_selective_scan_fwd",
     "packmamba_selective_scan_bwd_workspace_size", "packmamba_selective_scan_bwd",
     "packmamba_check_position_indices", "packmamba_pack_plan", "packmamba_pack_positions",
+    "packmamba_rmsnorm_fwd", "packmamba_rmsnorm_bwd_workspace_size", "packmamba_rmsnorm_bwd",
 )
 
 PACK_SEQUENTIAL, PACK_GREEDY, PACK_CUT = 0, 1, 2
@@ -75,10 +76,14 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.packmamba_check_position_indices.argtypes = [vp, i64, i64, i32, vp, vp]
     lib.packmamba_pack_plan.argtypes = [vp, i64, i64, i32, i64, vp, i64, vp, vp]
     lib.packmamba_pack_positions.argtypes = [vp, i64, i64, i64, vp]
+    lib.packmamba_rmsnorm_fwd.argtypes = [vp, vp, ctypes.c_float, vp, vp, i64, i64, i64, i32, vp]
+    lib.packmamba_rmsnorm_bwd_workspace_size.argtypes = [i64, i64, i64]
+    lib.packmamba_rmsnorm_bwd_workspace_size.restype = sz
+    lib.packmamba_rmsnorm_bwd.argtypes = [vp] * 8 + [sz, i64, i64, i64, i32, vp]
     for name in ("packmamba_pack_plan", "packmamba_pack_positions", "packmamba_causal_conv1d_fwd",
                  "packmamba_causal_conv1d_bwd",
                  "packmamba_selective_scan_fwd", "packmamba_selective_scan_bwd",
-                 "packmamba_check_position_indices"):
+                 "packmamba_check_position_indices", "packmamba_rmsnorm_fwd", "packmamba_rmsnorm_bwd"):
         getattr(lib, name).restype = ctypes.c_int
     if lib.packmamba_abi_version() != ABI_VERSION:
         raise RuntimeError("libpackmamba ABI version mismatch")

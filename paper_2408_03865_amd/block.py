@@ -2,10 +2,11 @@
 conv1d + SiLU, x and dt projections, packed selective scan with the D skip and the
 SiLU(z) gate, output projection, residual -- forward and backward.
 
-The sequence-wise steps (conv, scan) run in this library's HIP kernels through the C
-ABI; the projections are plain GEMMs, run by hipBLASLt through torch.matmul; RMSNorm
-and the residual are token-wise torch operations (§3.2: token-wise and element-wise
-operators satisfy PUI unchanged, so packing needs nothing from them).  Activations are
+The sequence-wise steps (conv, scan) and RMSNorm (with the residual's gradient
+folded into its backward) run in this library's HIP kernels through the C ABI; the
+projections are plain GEMMs, run by hipBLASLt through torch.matmul; the residual add
+of the forward is one torch addition (§3.2: token-wise and element-wise operators
+satisfy PUI unchanged, so packing needs nothing from them).  Activations are
 laid out (batch, features, seqlen), sequence innermost, which is the layout of the
 conv and scan kernels, so no transposes sit between the steps: each projection is a
 batched GEMM W @ X[b], split per output part so that every tensor the kernels see is
@@ -52,22 +53,6 @@ def _lin_dw(dY, Xt):
     return torch.matmul(dY2, Xt)
 
 
-def rmsnorm(x, w, eps=EPS):
-    torch = _torch()
-    xf = x.float()
-    r = torch.rsqrt(xf.pow(2).mean(1, keepdim=True) + eps)
-    return (xf * r * w[None, :, None]).to(x.dtype), r
-
-
-def rmsnorm_bwd(x, w, r, dh):
-    xh = x.float() * r
-    dhf = dh.float()
-    dw = (dhf * xh).sum((0, 2))
-    dxh = dhf * w[None, :, None]
-    dx = r * (dxh - xh * (dxh * xh).mean(1, keepdim=True))
-    return dx, dw
-
-
 def block_forward(x, pos, p: Dict[str, object], mark: Optional[Callable[[str], None]] = None):
     """out = x + W_out @ scan(conv(W_in,x @ RMSNorm(x)), ...): returns (out, ctx)."""
     mk = mark or (lambda name: None)
@@ -75,7 +60,7 @@ def block_forward(x, pos, p: Dict[str, object], mark: Optional[Callable[[str], N
     N = p["A"].shape[1]
     R = p["W_dt"].shape[1]
     mk("norm")
-    h, r = rmsnorm(x, p["norm_w"])
+    h, r = P.rmsnorm_fwd(x, p["norm_w"], EPS)
     mk("in_proj")
     xi = _lin(p["W_in"][:Dn], h)
     z = _lin(p["W_in"][Dn:], h)
@@ -128,7 +113,7 @@ def block_backward(dout, ctx, p, mark: Optional[Callable[[str], None]] = None) -
     g["W_in"] = _torch().cat([_lin_dw(dxi, ht), _lin_dw(s["dz"], ht)], 0)
     dh = _lin_dx(p["W_in"][:Dn], dxi) + _lin_dx(p["W_in"][Dn:], s["dz"])
     mk("norm_bwd")
-    dxn, g["norm_w"] = rmsnorm_bwd(ctx["x"], p["norm_w"], ctx["r"], dh)
-    g["x"] = (dout.float() + dxn).to(dt)
+    # the residual's gradient (dout itself) is added inside the RMSNorm backward
+    g["x"], g["norm_w"] = P.rmsnorm_bwd(ctx["x"], p["norm_w"], ctx["r"], dh, dresidual=dout)
     mk("end")
     return g

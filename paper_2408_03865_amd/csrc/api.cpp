@@ -253,6 +253,44 @@ int packmamba_selective_scan_bwd(const void* u, const void* delta, const float* 
     return launch_status(pm::launch_scan_bwd(a, s));
 }
 
+int packmamba_rmsnorm_fwd(const void* x, const float* weight, float eps, void* out, float* rstd,
+                          int64_t batch, int64_t dim, int64_t seqlen, int32_t dtype, void* stream) {
+    if (!x || !weight || !out || !rstd) return PACKMAMBA_ERR_NULL;
+    if (int e = check_shape(batch, dim, seqlen)) return e;
+    if (int e = check_dtype(dtype)) return e;
+    if (!(eps >= 0.0f)) return PACKMAMBA_ERR_SHAPE;
+    if (!aligned16(x) || !aligned16(weight) || !aligned16(out) || !aligned16(rstd)) return PACKMAMBA_ERR_ALIGN;
+    pm::RmsArgs a{};
+    a.x = x; a.w = weight; a.out = out; a.rstd_out = rstd; a.eps = eps;
+    a.batch = batch; a.dim = dim; a.seqlen = seqlen; a.dtype = dtype;
+    return launch_status(pm::launch_rmsnorm_fwd(a, (hipStream_t)stream));
+}
+
+size_t packmamba_rmsnorm_bwd_workspace_size(int64_t batch, int64_t dim, int64_t seqlen) {
+    if (check_shape(batch, dim, seqlen)) return 0;
+    const int64_t tiles = (seqlen + pm::kRmsTile - 1) / pm::kRmsTile;
+    return align_up(sizeof(float) * (size_t)(batch * tiles * dim));
+}
+
+int packmamba_rmsnorm_bwd(const void* x, const float* weight, const float* rstd, const void* dout,
+                          const void* dresidual, void* dx, float* dweight, void* workspace,
+                          size_t workspace_bytes, int64_t batch, int64_t dim, int64_t seqlen,
+                          int32_t dtype, void* stream) {
+    if (!x || !weight || !rstd || !dout || !dx || !dweight) return PACKMAMBA_ERR_NULL;
+    if (int e = check_shape(batch, dim, seqlen)) return e;
+    if (int e = check_dtype(dtype)) return e;
+    if (!aligned16(x) || !aligned16(weight) || !aligned16(rstd) || !aligned16(dout) ||
+        !aligned16(dresidual) || !aligned16(dx) || !aligned16(dweight) || !aligned16(workspace))
+        return PACKMAMBA_ERR_ALIGN;
+    const size_t need = packmamba_rmsnorm_bwd_workspace_size(batch, dim, seqlen);
+    if (!workspace || workspace_bytes < need) return PACKMAMBA_ERR_WORKSPACE;
+    pm::RmsArgs a{};
+    a.x = x; a.w = weight; a.rstd = rstd; a.dout = dout; a.dres = dresidual; a.out = dx;
+    a.dw = dweight; a.partial = static_cast<float*>(workspace);
+    a.batch = batch; a.dim = dim; a.seqlen = seqlen; a.dtype = dtype;
+    return launch_status(pm::launch_rmsnorm_bwd(a, (hipStream_t)stream));
+}
+
 int packmamba_check_position_indices(const int32_t* position_indices, int64_t batch,
                                      int64_t seqlen, int32_t continued, int32_t* d_flag,
                                      void* stream) {

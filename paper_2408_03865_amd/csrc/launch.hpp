@@ -30,6 +30,25 @@ struct ConvArgs {
 hipError_t launch_conv1d_fwd(const ConvArgs& a, hipStream_t s);
 hipError_t launch_conv1d_bwd(const ConvArgs& a, hipStream_t s);
 
+// RMSNorm over the feature axis of (batch, dim, seqlen) activations.
+constexpr int64_t kRmsTile = 64;     // tokens per block; one dweight partial per (batch, tile)
+struct RmsArgs {
+    const void* x;
+    const float* w;
+    const float* rstd;  // bwd: saved by the forward, (batch, seqlen)
+    const void* dout;   // bwd only
+    const void* dres;   // bwd only: gradient added to dx, or null
+    void* out;          // fwd: out; bwd: dx
+    float* rstd_out;    // fwd: (batch, seqlen)
+    float* dw;          // bwd only
+    float* partial;     // bwd only: (batch, tiles, dim)
+    float eps;
+    int64_t batch, dim, seqlen;
+    int32_t dtype;
+};
+hipError_t launch_rmsnorm_fwd(const RmsArgs& a, hipStream_t s);
+hipError_t launch_rmsnorm_bwd(const RmsArgs& a, hipStream_t s);
+
 // The conv backward runs one wave per (row, segment); a row is cut into segments of
 // whole 512-token steps when batch x dim alone gives fewer than kConvBwdWaves waves.
 constexpr int64_t kConvBwdSpan = 512;

@@ -26,7 +26,7 @@ def test_exports_every_declared_symbol():
     lib = _lib()
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.packmamba_abi_version() == 3
+    assert lib.packmamba_abi_version() == 4
 
 
 def test_status_strings():
@@ -146,3 +146,18 @@ def test_argument_errors_before_launch():
     assert bwd(*a) == 3
     assert lib.packmamba_check_position_indices(None, 1, 8, 0, P, None) == 1
     assert lib.packmamba_check_position_indices(U, 1, 8, 1, P, None) == 4
+    # RMSNorm
+    nf, nb = lib.packmamba_rmsnorm_fwd, lib.packmamba_rmsnorm_bwd
+    assert nf(None, P, 1e-5, P, P, 1, 4, 8, 0, None) == 1
+    assert nf(P, P, 1e-5, P, None, 1, 4, 8, 0, None) == 1
+    assert nf(P, P, 1e-5, P, P, 0, 4, 8, 0, None) == 2
+    assert nf(P, P, -1.0, P, P, 1, 4, 8, 0, None) == 2
+    assert nf(P, P, float("nan"), P, P, 1, 4, 8, 0, None) == 2
+    assert nf(P, P, 1e-5, P, P, 1, 4, 8, 9, None) == 3
+    assert nf(U, P, 1e-5, P, P, 1, 4, 8, 0, None) == 4
+    ws = lib.packmamba_rmsnorm_bwd_workspace_size(2, 4, 100)
+    assert ws >= 2 * 2 * 4 * 4 and lib.packmamba_rmsnorm_bwd_workspace_size(0, 4, 100) == 0
+    assert nb(P, P, P, P, None, P, None, P, ws, 2, 4, 100, 0, None) == 1                # no dweight
+    assert nb(P, P, P, P, None, P, P, P, ws - 1, 2, 4, 100, 0, None) == 5
+    assert nb(P, P, P, P, U, P, P, P, ws, 2, 4, 100, 0, None) == 4                     # dresidual
+    assert nb(P, P, P, P, None, P, P, P, ws, 2, 4, 100, 5, None) == 3
