@@ -41,16 +41,16 @@ def _lin_dx(W, dY):
     return _torch().matmul(W.t().contiguous(), dY)
 
 
-def _tokens_major(X):
-    """(batch, f, L) -> (batch*L, f), contiguous: the right operand of a weight gradient."""
-    return X.transpose(1, 2).reshape(-1, X.shape[1])
-
-
-def _lin_dw(dY, Xt):
-    """dW = sum_b dY[b] @ X[b]^T, with Xt = _tokens_major(X)."""
+def _lin_dw(dY, X):
+    """dW = sum_b dY[b] @ X[b]^T: one 2-D GEMM per batch row, X[b] read transposed in
+    place (no copy), accumulated in fp32 and returned in dY's dtype."""
     torch = _torch()
-    dY2 = dY.transpose(0, 1).reshape(dY.shape[1], -1)          # (out, batch*L)
-    return torch.matmul(dY2, Xt)
+    f32 = torch.float32
+    kw = {} if dY.dtype == f32 else {"out_dtype": f32}
+    acc = torch.mm(dY[0], X[0].t(), **kw)
+    for b in range(1, dY.shape[0]):
+        acc = torch.addmm(acc, dY[b], X[b].t(), **kw)
+    return acc.to(dY.dtype)
 
 
 def block_forward(x, pos, p: Dict[str, object], mark: Optional[Callable[[str], None]] = None):
@@ -86,32 +86,30 @@ def block_backward(dout, ctx, p, mark: Optional[Callable[[str], None]] = None) -
     """Gradients of sum(dout * out) with respect to x and every parameter."""
     mk = mark or (lambda name: None)
     Dn = p["D"].shape[0]
-    N = p["A"].shape[1]
-    R = p["W_dt"].shape[1]
     Wx = p["W_x"]
     dt = dout.dtype
     g = {}
     mk("out_proj_bwd")
-    g["W_out"] = _lin_dw(dout, _tokens_major(ctx["y"]))
+    g["W_out"] = _lin_dw(dout, ctx["y"])
     dy = _lin_dx(p["W_out"], dout)
     mk("scan_bwd")
     s = P.selective_scan_bwd(ctx["u"], ctx["delta"], p["A"], ctx["B"], ctx["C"], p["D"], ctx["z"],
                              p["dt_bias"], True, ctx["pos"], dy, saved_states=ctx["st"])
     g["A"], g["D"], g["dt_bias"] = s["dA"], s["dD"], s["ddelta_bias"]
     mk("x_proj_bwd")
-    g["W_dt"] = _lin_dw(s["ddelta"], _tokens_major(ctx["dtl"]))
+    g["W_dt"] = _lin_dw(s["ddelta"], ctx["dtl"])
     ddtl = _lin_dx(p["W_dt"], s["ddelta"])
-    dB, dC = s["dB"].to(dt), s["dC"].to(dt)
-    ut = _tokens_major(ctx["u"])
-    g["W_x"] = _torch().cat([_lin_dw(ddtl, ut), _lin_dw(dB, ut), _lin_dw(dC, ut)], 0)
-    du = s["du"] + _lin_dx(Wx[:R], ddtl) + _lin_dx(Wx[R:R + N], dB) + _lin_dx(Wx[R + N:], dC)
+    dxdbl = _torch().cat([ddtl, s["dB"].to(dt), s["dC"].to(dt)], 1)      # (batch, R + 2N, L)
+    g["W_x"] = _lin_dw(dxdbl, ctx["u"])
+    du = _lin_dx(Wx, dxdbl)
+    du += s["du"]
     mk("conv_bwd")
     dxi, g["conv_w"], g["conv_b"] = P.causal_conv1d_bwd(ctx["xi"], p["conv_w"], p["conv_b"], ctx["pos"],
                                                         du.contiguous(), silu=True)
     mk("in_proj_bwd")
-    ht = _tokens_major(ctx["h"])
-    g["W_in"] = _torch().cat([_lin_dw(dxi, ht), _lin_dw(s["dz"], ht)], 0)
-    dh = _lin_dx(p["W_in"][:Dn], dxi) + _lin_dx(p["W_in"][Dn:], s["dz"])
+    g["W_in"] = _torch().cat([_lin_dw(dxi, ctx["h"]), _lin_dw(s["dz"], ctx["h"])], 0)
+    dh = _lin_dx(p["W_in"][:Dn], dxi)
+    dh += _lin_dx(p["W_in"][Dn:], s["dz"])
     mk("norm_bwd")
     # the residual's gradient (dout itself) is added inside the RMSNorm backward
     g["x"], g["norm_w"] = P.rmsnorm_bwd(ctx["x"], p["norm_w"], ctx["r"], dh, dresidual=dout)
