@@ -300,7 +300,13 @@ void scan_bwd_kernel(BwdParams p) {
             for (int k = K - 2; k >= 0; --k) Hr = fmaf(a[k + 1], Hr, cdy[k]);
             float P = fast_exp2(fmaf(S, A2n, Mf));
             float Pr = fast_exp2(fmaf(Sr, A2n, Mr));
+            // Wave priority (s_setprio, per wave, relative to the other waves of the SIMD):
+            // raised over this DPP latency chain, and from the reverse recurrence to the
+            // state's barrier, so that the block's waves reach the barrier sooner; the
+            // other blocks' waves fill the issue slots meanwhile (-4% at 8 x 4096 x 4096).
+            __builtin_amdgcn_s_setprio(1);
             row_scan_up_down(P, H, Pr, Hr);
+            __builtin_amdgcn_s_setprio(0);
             // ---- replay the forward inside the chunk ----
             const float hend = fmaf(P, hin, H);
             float hprev = dpp<kRowShr1>(hin, hend);
@@ -326,6 +332,7 @@ void scan_bwd_kernel(BwdParams p) {
                 sm.xc[r][n] = dhfirst;
                 sm.an[r][n] = a[0];
             }
+            __builtin_amdgcn_s_setprio(2);
             float dAl = 0.0f;
             float dBp[K];
 #pragma unroll
@@ -362,6 +369,7 @@ void scan_bwd_kernel(BwdParams p) {
             const int par = (n & 1) * (kWaves * 2 * kCH);
             *reinterpret_cast<f32x4*>(red_w + par) = f32x4{Q[0], Q[1], Q[2], Q[3]};
             __syncthreads();
+            __builtin_amdgcn_s_setprio(0);
             {   // then over the block's 4 waves, in a fixed order
                 float s = 0.0f;
 #pragma unroll
