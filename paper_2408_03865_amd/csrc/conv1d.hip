@@ -1,14 +1,16 @@
 // conv1d.hip -- packed causal depthwise conv1d, forward and backward (Alg. 1, §3.3, §3.5).
 //
-// HBM-bound streaming kernels.  One 256-thread block per (batch, channel) row;
-// each thread owns 8 consecutive tokens per step (one 16-byte vector of bf16,
-// two of fp32) and loops along the row.  The width-1 halo comes from the
-// neighbouring vector, which the neighbouring lane loads in the same instruction,
-// so it is served by the cache and costs no extra HBM traffic.  The tap mask
-// uses only integer compares against the token's position index, read with the
-// same coalesced vector loads (§3.5): the forward keeps the tap reaching k tokens
-// back iff k <= pos[l]; the backward's dx reads the next width-1 tokens'
-// indices ("reverse indices") and keeps tap k iff pos[j+k] >= k.
+// HBM-bound streaming kernels.  The tap mask uses only integer compares against
+// the token's position index, read with the same coalesced vector loads (§3.5):
+// the forward keeps the tap reaching k tokens back iff k <= pos[l]; the
+// backward's dx takes the next width-1 tokens' indices ("reverse indices") and
+// keeps tap k iff pos[j+k] >= k.
+//  - Forward: one 256-thread block per (batch, channel) row; each thread owns 8
+//    consecutive tokens per step (one 16-byte vector of bf16, two of fp32) and
+//    loops along the row.  The width-1 halo comes from the neighbouring vector,
+//    which the neighbouring lane loads in the same instruction, so it is served by
+//    the cache and costs no extra HBM traffic.
+//  - Backward: one wave per (row, segment), described at its kernel.
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -108,30 +110,6 @@ __global__ __launch_bounds__(kThreads) void conv1d_fwd_kernel(
             if (m >= 0) v = xr[m];
             else if (st.xinit) v = st.xinit[row * (W - 1) + (W - 1) + m];
             st.xfinal[row * (W - 1) + i] = v;
-        }
-    }
-}
-
-// Block-wide sum of NV values per thread; thread 0 receives the totals.
-template <int NV>
-__device__ __forceinline__ void block_sum(float* v, float* lds /* NV * (kThreads/64) */) {
-#pragma unroll
-    for (int j = 0; j < NV; ++j) {
-#pragma unroll
-        for (int off = 32; off >= 1; off >>= 1) v[j] += __shfl_xor(v[j], off, 64);
-    }
-    const int wave = threadIdx.x >> 6;
-    if ((threadIdx.x & 63) == 0) {
-#pragma unroll
-        for (int j = 0; j < NV; ++j) lds[j * (kThreads / 64) + wave] = v[j];
-    }
-    __syncthreads();
-    if (threadIdx.x == 0) {
-#pragma unroll
-        for (int j = 0; j < NV; ++j) {
-            float s = 0.0f;
-            for (int q = 0; q < kThreads / 64; ++q) s += lds[j * (kThreads / 64) + q];
-            v[j] = s;
         }
     }
 }
