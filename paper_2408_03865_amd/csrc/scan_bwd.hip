@@ -449,7 +449,6 @@ struct __attribute__((aligned(16))) AggSmem {
     float A2[kRows][kN];
     float xc[kRows][kN];
     float q[kRows][kN];
-    int first_start;
 };
 
 template <typename T>
@@ -469,7 +468,7 @@ __global__ __launch_bounds__(kThreads) void scan_bwd_agg_kernel(BwdParams p) {
     const int64_t rowoff = (b * p.dim + d) * L;
     const int64_t nchunk = (L + kCH - 1) / kCH;
     const int64_t c0 = (int64_t)seg * p.seg_chunks;
-    int64_t c1 = min(nchunk, c0 + p.seg_chunks);
+    const int64_t c1 = min(nchunk, c0 + p.seg_chunks);
 
     const T* dr = static_cast<const T*>(p.delta) + rowoff;
     const T* zr = p.z ? static_cast<const T*>(p.z) + rowoff : nullptr;
@@ -477,39 +476,7 @@ __global__ __launch_bounds__(kThreads) void scan_bwd_agg_kernel(BwdParams p) {
     const T* Cb = static_cast<const T*>(p.C) + b * kN * L;
     const int32_t* pr = p.pos + b * L;
 
-    // dh at the segment's first token does not depend on the tokens from the first
-    // sequence start after it on (the multiplier into that start is 0), so the
-    // aggregate ends at the chunk holding the token before that start.
-    {
-        const int64_t ls = c0 * kCH;
-        const int64_t le = min(c1 * kCH, L);
-        const int64_t st = (le - 1) - (int64_t)pr[le - 1];
-        if (st > ls) {                       // some start lies in (ls, le): find the first
-            constexpr int kNone = 0x7fffffff;
-            if (tid == 0) sm.first_start = kNone;
-            __syncthreads();
-            for (int64_t base = ls + 1; base < le; base += kThreads * 4) {
-                int found = kNone;
-#pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    const int64_t l = base + tid * 4 + k;
-                    if (l < le && found == kNone && pr[l] == 0) found = (int)l;
-                }
-                if (found != kNone) atomicMin(&sm.first_start, found);
-                __syncthreads();
-                const int v = sm.first_start;
-                __syncthreads();                 // every thread has read v before any new atomic
-                if (v != kNone) {
-                    c1 = min(c1, (int64_t)(v - 1) / kCH + 1);
-                    break;
-                }
-            }
-        }
-    }
-
     const float dbias = p.delta_bias ? p.delta_bias[d] : 0.0f;
-    float dt_next, m_next;
-    token_step<T>(dr, pr, c1 * kCH, L, dbias, p.softplus, dt_next, m_next);
     {
         const int rr = tid >> 4, n = tid & 15;
         const int64_t dd = min(g * kRows + rr, p.dim - 1);
@@ -521,6 +488,8 @@ __global__ __launch_bounds__(kThreads) void scan_bwd_agg_kernel(BwdParams p) {
     auto chunk = [&](auto full_tag, const int64_t c) {
         constexpr bool FULL = decltype(full_tag)::value;
         const int64_t lb = c * kCH;
+        float dt_next, m_next;     // step and mask of the first token after the chunk
+        token_step<T>(dr, pr, lb + kCH, L, dbias, p.softplus, dt_next, m_next);
         for (int idx = tid * PV; idx < kN * kCH; idx += kThreads * PV) {
             const int n = idx / kCH, t = idx - n * kCH;
             float vc[PV];
@@ -571,13 +540,10 @@ __global__ __launch_bounds__(kThreads) void scan_bwd_agg_kernel(BwdParams p) {
         const float m0n = dpp<kRowShl1>(m_next, M[0]);
         const float Sr = S - dt[0] + dt0n;
         Mr += m0n;
-        dt_next = dpp<kNewBcast0>(0.0f, dt[0]);
-        m_next = dpp<kNewBcast0>(0.0f, M[0]);
 
 #pragma unroll 1
         for (int n = 0; n < kN; ++n) {
             const float A2n = sm.A2[r][n];
-            const float xc = sm.xc[r][n];
             float cdy[K];
 #pragma unroll
             for (int k = 0; k < K; k += 4) {
@@ -591,16 +557,25 @@ __global__ __launch_bounds__(kThreads) void scan_bwd_agg_kernel(BwdParams p) {
                 Hr = fmaf(fast_exp2(fmaf(dt[k + 1], A2n, M[k + 1])), Hr, cdy[k]);
             float Pr = fast_exp2(fmaf(Sr, A2n, Mr));
             row_scan_down(Pr, Hr);
+            // lane 0's (Pr, Hr) is the chunk's map from dh after the chunk to dh at its
+            // first token; the chunks before it are already composed in (q, xc), which
+            // becomes (q Pr, q Hr + xc)
             if (j == 0) {
-                sm.xc[r][n] = fmaf(Pr, xc, Hr);
-                sm.q[r][n] *= Pr;                 // lane 0's Pr spans the chunk
+                const float qa = sm.q[r][n];
+                sm.xc[r][n] = fmaf(qa, Hr, sm.xc[r][n]);
+                sm.q[r][n] = qa * Pr;
             }
         }
         __syncthreads();
     };
-    for (int64_t c = c1 - 1; c >= c0; --c) {
+    // The chunk maps are composed from the segment's start forwards.  Once the product
+    // of the multipliers is exactly 0 for every channel and state of the block (the
+    // token before a sequence start, or underflow of a long decay), the later chunks
+    // contribute exactly nothing, and the walk stops.
+    for (int64_t c = c0; c < c1; ++c) {
         if (p.vec && (c + 1) * kCH <= L) chunk(std::true_type{}, c);
         else chunk(std::false_type{}, c);
+        if (!__syncthreads_or(sm.q[tid >> 4][tid & 15] != 0.0f)) break;
     }
     {
         const int rr = tid >> 4, n = tid & 15;

@@ -200,13 +200,19 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_kernel(FwdParams p) {
             for (int k = 1; k < K; ++k) H = fmaf(a[k], H, bx[k]);
             float P = fast_exp2(fmaf(S, A2n, Mf));
             row_scan_up(P, H);
+            if (AGG) {
+                // lane 15's (P, H) is the chunk's map; the chunks after it are already
+                // composed in (pseg, carry), which becomes (pseg P, pseg H + carry)
+                if (j == 15) {
+                    const float pa = sm.pseg[r][n];
+                    sm.carry[r][n] = fmaf(pa, H, sm.carry[r][n]);
+                    sm.pseg[r][n] = pa * P;
+                }
+                continue;
+            }
             const float hend = fmaf(P, cin, H);               // state after this lane's last token
             float h = dpp<kRowShr1>(cin, hend);               // state before this lane's first token
-            if (j == 15) {
-                sm.carry[r][n] = hend;                        // state after the chunk
-                if (AGG) sm.pseg[r][n] *= P;                  // lane 15's P spans the chunk
-            }
-            if (AGG) continue;
+            if (j == 15) sm.carry[r][n] = hend;               // state after the chunk
 #pragma unroll
             for (int k = 0; k < K; k += 4) {
                 const f32x4 cv = *reinterpret_cast<const f32x4*>(&sm.C[n][j][k]);
@@ -239,17 +245,21 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_kernel(FwdParams p) {
     };
     const int64_t c0 = (int64_t)seg * p.seg_chunks;
     const int64_t c1 = min(nchunk, c0 + p.seg_chunks);
-    int64_t cs = c0;
     if (AGG) {
-        // The segment's map is unchanged by the chunks before the last sequence start
-        // inside it (that start's multiplier is 0), so the aggregate begins there.
-        const int64_t le = min(c1 * CH, L) - 1;
-        const int64_t st = le - (int64_t)pr[le];      // start of the sequence holding token le
-        if (st > c0 * CH) cs = min(st / CH, c1 - 1);
-    }
-    for (int64_t c = cs; c < c1; ++c) {
-        if (p.vec && (c + 1) * CH <= L) chunk(std::true_type{}, c);
-        else chunk(std::false_type{}, c);
+        // The aggregate composes the chunk maps from the segment's end backwards.  Once
+        // the product of the multipliers is exactly 0 for every channel and state of the
+        // block (a sequence start, or underflow of a long decay), the earlier chunks
+        // contribute exactly nothing, and the walk stops.
+        for (int64_t c = c1 - 1; c >= c0; --c) {
+            if (p.vec && (c + 1) * CH <= L) chunk(std::true_type{}, c);
+            else chunk(std::false_type{}, c);
+            if (!__syncthreads_or(sm.pseg[tid >> 4][tid & 15] != 0.0f)) break;
+        }
+    } else {
+        for (int64_t c = c0; c < c1; ++c) {
+            if (p.vec && (c + 1) * CH <= L) chunk(std::true_type{}, c);
+            else chunk(std::false_type{}, c);
+        }
     }
     if (AGG) {
         __syncthreads();
