@@ -142,9 +142,9 @@ def segments(batch: int, dim: int, seqlen: int) -> int:
     the rule of the library's launchers, for tests and reports only."""
     blocks = batch * ((dim + 15) // 16)
     units = (seqlen + 255) // 256
-    if blocks >= 768 or units < 2:
+    if blocks * 2 >= 1536 or units < 2:
         return 1
-    nseg = min((768 + blocks - 1) // blocks, units)
+    nseg = min((1536 + blocks - 1) // blocks, units)
     per = (units + nseg - 1) // nseg
     return (units + per - 1) // per
 

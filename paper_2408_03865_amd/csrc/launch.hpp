@@ -106,21 +106,19 @@ constexpr int kScanBwdChannels = 16;
 
 // Split of the rows into segments along the sequence, each scanned by its own
 // block with the carry across segments resolved by an aggregate pass and a carry
-// pass.  Used only when batch x (channel groups of 16) does not fill one round of
-// the GPU (256 CUs hold three scan blocks each); the rows are then cut into the
-// fewest segments that fill it (measured faster than two rounds' worth: the
-// aggregate pass costs more than the extra occupancy gains).
+// pass.  Used only when batch x (channel groups of 16) leaves the GPU underfilled:
+// 256 CUs hold three scan blocks each, and two blocks per slot are wanted.
 struct SegPlan {
     int64_t nseg;      // segments per row (1: no split)
     int64_t seg_len;   // tokens per segment, a multiple of kSegUnit
 };
 constexpr int64_t kSegUnit = 256;          // forward chunk, a multiple of the backward chunk
-constexpr int64_t kSegTargetBlocks = 768;
+constexpr int64_t kSegTargetBlocks = 1536;
 
 inline SegPlan scan_segments(int64_t batch, int64_t dim, int64_t seqlen) {
     const int64_t blocks = batch * ((dim + 15) / 16);
     const int64_t units = (seqlen + kSegUnit - 1) / kSegUnit;
-    if (blocks >= kSegTargetBlocks || units < 2) return {1, units * kSegUnit};
+    if (blocks * 2 >= kSegTargetBlocks || units < 2) return {1, units * kSegUnit};
     int64_t nseg = (kSegTargetBlocks + blocks - 1) / blocks;
     if (nseg > units) nseg = units;
     const int64_t per = (units + nseg - 1) / nseg;

@@ -48,7 +48,7 @@ def test_sizes():
     # forward workspace: only for shapes whose rows are split into segments
     assert lib.packmamba_selective_scan_fwd_workspace_size(8, 4096, 4096, 16) == 0
     assert lib.packmamba_selective_scan_fwd_workspace_size(1, 2048, 256, 16) == 0      # one 256-token unit
-    assert lib.packmamba_selective_scan_fwd_workspace_size(1, 2048, 65536, 16) >= 1 * 2048 * 6 * 16 * 12
+    assert lib.packmamba_selective_scan_fwd_workspace_size(1, 2048, 65536, 16) >= 1 * 2048 * 12 * 16 * 12
     assert lib.packmamba_selective_scan_fwd_workspace_size(0, 2048, 65536, 16) == 0
     assert (lib.packmamba_selective_scan_bwd_workspace_size(1, 2048, 65536, 16)
             > lib.packmamba_selective_scan_fwd_workspace_size(1, 2048, 65536, 16))
@@ -68,9 +68,9 @@ def test_segment_rule():
             b, d, _ = shape
             assert ws >= b * d * ns * 16 * 12, shape
     assert P.segments(8, 4096, 4096) == 1
-    assert P.segments(1, 2048, 65536) == 6
-    assert P.segments(2, 2048, 8192) == 3
-    assert P.segments(4, 1536, 2048) == 2
+    assert P.segments(1, 2048, 65536) == 12
+    assert P.segments(2, 2048, 8192) == 6
+    assert P.segments(4, 1536, 2048) == 4
 
 
 def _gpu_visible():
