@@ -1,0 +1,38 @@
+"""Seeded random shapes and options against the oracle: batch, channel count (not
+multiples of the 16-channel blocks), row length (ragged against the 8-token
+vectors, the 128/256-token chunks and the 512-token conv steps, long enough to be
+split into segments or not), conv width, dtype, length law (from all-length-1 rows
+to one sequence per row) and A recipe.  Every output and gradient of both operators
+is compared element by element."""
+import numpy as np
+import pytest
+
+import workloads as W
+from gpu_common import PER_B, PER_CHANNEL, PER_TOKEN, TOL, compare, gpu_inputs, note, oracle_run, run_gpu
+
+pytestmark = pytest.mark.gpu
+
+ALL = PER_TOKEN + PER_CHANNEL + PER_B
+
+
+def _case(i):
+    rng = np.random.default_rng(9100 + i)
+    batch = int(rng.integers(1, 5))
+    dim = int(rng.integers(1, 71))
+    seqlen = int(rng.choice([1, 7, 64, 129, 255, 513, 1000, 2049, 3001]))
+    width = int(rng.integers(2, 5))
+    dtype = ["f32", "bf16"][i % 2]
+    law = [("lognormal", 2.0, 1.5, 1, seqlen), ("lognormal", 6.0, 1.0, 1, seqlen),
+           ("lognormal", 0.0, 0.1, 1, 1), ("edges", 1, 64), ("arange",)][int(rng.integers(0, 5))]
+    variant = ["paper", "general"][int(rng.integers(0, 2))]
+    return batch, dim, seqlen, width, dtype, law, variant
+
+
+@pytest.mark.parametrize("i", range(12))
+def test_random_case(i):
+    batch, dim, seqlen, width, dtype, law, variant = _case(i)
+    note(f"random case {i}: batch {batch} dim {dim} seqlen {seqlen} width {width} {dtype} {law} {variant}")
+    cfg = W.Config("random", "random", batch, seqlen, dim, 16, width, dtype, law, 9200 + i)
+    d = W.make_inputs(cfg, variant=variant)
+    r = run_gpu(gpu_inputs(d, dtype), out_f32=(dtype == "bf16"))
+    compare(r, oracle_run(d), TOL[dtype], ALL, label=f"random {i} ")
