@@ -543,6 +543,9 @@ __global__ __launch_bounds__(kThreads) void scan_bwd_agg_kernel(BwdParams p) {
 
 #pragma unroll 1
         for (int n = 0; n < kN; ++n) {
+            // a (channel, state) whose multiplier product is already exactly 0 is final;
+            // the wave skips the state when that holds for its 4 channels
+            if (__all(sm.q[r][n] == 0.0f)) continue;
             const float A2n = sm.A2[r][n];
             float cdy[K];
 #pragma unroll

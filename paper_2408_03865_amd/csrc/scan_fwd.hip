@@ -181,6 +181,9 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_kernel(FwdParams p) {
         // ---- states ----
 #pragma unroll 1
         for (int n = 0; n < kN; ++n) {
+            // aggregate: a (channel, state) whose multiplier product is already exactly 0
+            // is final; the wave skips the state when that holds for its 4 channels
+            if (AGG && __all(sm.pseg[r][n] == 0.0f)) continue;
             const float A2n = sm.A2[r][n];
             const float cin = sm.carry[r][n];
             float a[K], bx[K];
