@@ -112,6 +112,8 @@ __device__ __forceinline__ void unpack_run(const RawRun<T, K>& r, float* v) {
 }
 
 // Store K consecutive elements (rounding to T) at row[l0]; elements beyond L are dropped.
+// The vector stores are non-temporal: every output here is streamed out once, and
+// keeping it out of the caches leaves them to the inputs that are read again.
 template <typename T, int K, bool FULL = false>
 __device__ __forceinline__ void store_run(T* __restrict__ row, int64_t l0, int64_t L, bool vec,
                                           const float* v) {
@@ -119,7 +121,7 @@ __device__ __forceinline__ void store_run(T* __restrict__ row, int64_t l0, int64
     if (FULL || (vec && l0 + K <= L)) {
 #pragma unroll
         for (int i = 0; i < K / PV; ++i)
-            *reinterpret_cast<u32x4*>(row + l0 + i * PV) = Storage<T>::pack(v + i * PV);
+            __builtin_nontemporal_store(Storage<T>::pack(v + i * PV), reinterpret_cast<u32x4*>(row + l0 + i * PV));
     } else {
 #pragma unroll
         for (int i = 0; i < K; ++i)

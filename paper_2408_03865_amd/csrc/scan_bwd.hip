@@ -374,7 +374,7 @@ void scan_bwd_kernel(BwdParams p) {
                 float s = 0.0f;
 #pragma unroll
                 for (int q = 0; q < kWaves; ++q) s += red_r[par + q * 2 * kCH];
-                if (FULL || lb + red_t < L) part_n[n * L + part_off] = s;
+                if (FULL || lb + red_t < L) __builtin_nontemporal_store(s, &part_n[n * L + part_off]);   // read once, by the finalize
             }
             // no second barrier: the next state writes the other buffer, and this one is
             // rewritten only after every thread has passed the next state's barrier
