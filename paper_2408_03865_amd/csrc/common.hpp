@@ -112,16 +112,23 @@ __device__ __forceinline__ void unpack_run(const RawRun<T, K>& r, float* v) {
 }
 
 // Store K consecutive elements (rounding to T) at row[l0]; elements beyond L are dropped.
-// The vector stores are non-temporal: every output here is streamed out once, and
-// keeping it out of the caches leaves them to the inputs that are read again.
+// When a lane's K elements are one 16-byte vector, a wave's store covers 1 KB of
+// consecutive bytes, and the store is non-temporal: every output here is streamed
+// out once, and keeping it out of the caches leaves them to the inputs that are read
+// again.  With more vectors per lane each store covers every other 16 bytes of its
+// range; such partial lines are left to the caches to combine (no gain was measured
+// from making them non-temporal).
 template <typename T, int K, bool FULL = false>
 __device__ __forceinline__ void store_run(T* __restrict__ row, int64_t l0, int64_t L, bool vec,
                                           const float* v) {
     constexpr int PV = Storage<T>::kPerVec;
     if (FULL || (vec && l0 + K <= L)) {
 #pragma unroll
-        for (int i = 0; i < K / PV; ++i)
-            __builtin_nontemporal_store(Storage<T>::pack(v + i * PV), reinterpret_cast<u32x4*>(row + l0 + i * PV));
+        for (int i = 0; i < K / PV; ++i) {
+            u32x4* dst = reinterpret_cast<u32x4*>(row + l0 + i * PV);
+            if constexpr (K == PV) __builtin_nontemporal_store(Storage<T>::pack(v + i * PV), dst);
+            else *dst = Storage<T>::pack(v + i * PV);
+        }
     } else {
 #pragma unroll
         for (int i = 0; i < K; ++i)
