@@ -419,7 +419,7 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}, WORLD_SIZE {world}); "
-              "this build has no multi-GPU path.", file=sys.stderr)
+              "the path is single-GPU; rows would be split across ranks, one process per GPU.", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
