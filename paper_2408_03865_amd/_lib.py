@@ -9,6 +9,7 @@ from __future__ import annotations
 
 import ctypes
 import os
+from typing import Optional
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libpackmamba.so")
@@ -49,13 +50,24 @@ class PackMambaError(RuntimeError):
 _lib = None
 
 
-def load(path: str = LIB_PATH) -> ctypes.CDLL:
-    """Load the HIP library (raises if it is absent: build with paper_2408_03865_amd/build.py)."""
+def load(path: Optional[str] = None) -> ctypes.CDLL:
+    """Load the HIP library (raises if it is absent: build with paper_2408_03865_amd/build.py).
+    Without a path, the library named by LIB_PATH when the call is made, loaded once."""
     global _lib
+    if path is None:
+        path = LIB_PATH
     if _lib is not None and path == LIB_PATH:
         return _lib
     if not os.path.exists(path):
         raise FileNotFoundError(f"{path} is missing; build it with `python paper_2408_03865_amd/build.py`")
+    # One HIP runtime per process: torch ships its own libamdhip64.so.7, and the library's
+    # dependency of that name resolves to torch's copy only when torch is loaded first.
+    # The other way round the process holds two runtimes, and launches on torch's streams
+    # fail.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     lib = ctypes.CDLL(path)
     vp, i64, i32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
     lib.packmamba_abi_version.restype = ctypes.c_int

@@ -161,3 +161,20 @@ def test_argument_errors_before_launch():
     assert nb(P, P, P, P, None, P, P, P, ws - 1, 2, 4, 100, 0, None) == 5
     assert nb(P, P, P, P, U, P, P, P, ws, 2, 4, 100, 0, None) == 4                     # dresidual
     assert nb(P, P, P, P, None, P, P, P, ws, 2, 4, 100, 5, None) == 3
+
+
+def test_one_hip_runtime_per_process():
+    """Loading the library first must not put a second HIP runtime next to torch's own:
+    launches on torch's streams fail in such a process."""
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    code = ("import sys; sys.path.insert(0, %r)\n"
+            "from paper_2408_03865_amd import _lib\n"
+            "_lib.load()\n"
+            "import torch\n"
+            "maps = open('/proc/self/maps').read().splitlines()\n"
+            "print(len({l.split()[-1] for l in maps if 'libamdhip64' in l}))\n") % root
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0, r.stderr
+    assert r.stdout.strip().splitlines()[-1] == "1"
