@@ -108,8 +108,8 @@ class Chain:
         self.dB = torch.empty((Nb, N, L), dtype=torch.float32, device=dev)
         self.dC = torch.empty_like(self.dB)
         self.dw, self.dcb = torch.empty_like(t["w"]), torch.empty_like(t["bias"])
-        nst = (L + _lib.STATE_STRIDE - 1) // _lib.STATE_STRIDE
-        self.states = torch.empty((Nb, Dn, nst, N), dtype=torch.float32, device=dev)
+        nsaved = lib.packmamba_selective_scan_fwd_saved_states_size(Nb, Dn, L, N) // 4
+        self.states = torch.empty(nsaved, dtype=torch.float32, device=dev)
 
         def ws(n):
             return torch.empty(max(1, int(n)), dtype=torch.uint8, device=dev)

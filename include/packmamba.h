@@ -54,7 +54,7 @@
 extern "C" {
 #endif
 
-#define PACKMAMBA_ABI_VERSION 4
+#define PACKMAMBA_ABI_VERSION 5
 
 /* dtype codes of the activation tensors */
 #define PACKMAMBA_F32 0            /* fp32 inputs, fp32 outputs */
@@ -126,8 +126,11 @@ int packmamba_causal_conv1d_bwd(const void* x, const float* weight, const float*
                                 int64_t batch, int64_t dim, int64_t seqlen, int32_t width,
                                 int32_t dtype, int32_t silu, void* stream);
 
-/* Bytes of the optional saved-states buffer of packmamba_selective_scan_fwd:
- * (batch, dim, ceil(seqlen / PACKMAMBA_STATE_STRIDE), dstate) floats. */
+/* Bytes of the optional saved-states buffer of packmamba_selective_scan_fwd: the
+ * chunk states, (batch, dim, ceil(seqlen / PACKMAMBA_STATE_STRIDE), dstate) floats,
+ * then (batch, dim, seqlen rounded up to a multiple of 256) floats for the
+ * backward's dz, in an order of the library's own, starting at the first multiple
+ * of 256 bytes after the chunk states. */
 size_t packmamba_selective_scan_fwd_saved_states_size(int64_t batch, int64_t dim, int64_t seqlen,
                                                       int32_t dstate);
 
@@ -151,7 +154,9 @@ size_t packmamba_selective_scan_fwd_workspace_size(int64_t batch, int64_t dim, i
  *   saved_states: NULL, or a float buffer of
  *   packmamba_selective_scan_fwd_saved_states_size() bytes that receives h after
  *   token min((c+1)*PACKMAMBA_STATE_STRIDE, seqlen)-1 for every chunk c, laid out
- *   (batch, dim, chunk, dstate); the backward reuses it instead of recomputing.
+ *   (batch, dim, chunk, dstate), and, when z is given, (y + D u) times the
+ *   derivative of z sigmoid(z) for every token after it: the factor of dout in dz.
+ *   The backward reuses both instead of recomputing them.
  *   `out` may be NULL when saved_states or final_state is not (states only).
  *   initial_state: NULL (zeros), or (batch, dim, dstate) float: h before each row.
  *   final_state: NULL, or (batch, dim, dstate) float, receives h after each row.
@@ -182,7 +187,8 @@ size_t packmamba_selective_scan_bwd_workspace_size(int64_t batch, int64_t dim, i
  *   Inputs: as the forward, same order (initial_state included), plus dout
  *   (dtype), dfinal_state (NULL: zero; else the gradient of final_state,
  *   (batch, dim, dstate) float, entering h after the row's last token) and
- *   saved_states (NULL: recomputed into the workspace).
+ *   saved_states (NULL: recomputed into the workspace; else as written by the forward
+ *   on the same inputs).
  *   Outputs (overwritten): du, ddelta (dtype, like u); dA (dim, dstate);
  *   dB, dC (batch, dstate, seqlen) float; dD (dim) iff D != NULL;
  *   dz (dtype) iff z != NULL; ddelta_bias (dim) iff delta_bias != NULL;

@@ -30,7 +30,8 @@ from ._lib import BF16, BF16_F32OUT, F32, STATE_STRIDE, PackMambaError, load
 
 __all__ = [
     "causal_conv1d_fwd", "causal_conv1d_bwd", "selective_scan_fwd", "selective_scan_bwd",
-    "check_position_indices", "saved_states_size", "segments", "pack_plan", "pack_positions",
+    "check_position_indices", "saved_states_size", "chunk_states", "segments", "pack_plan",
+    "pack_positions",
     "rmsnorm_fwd", "rmsnorm_bwd",
     "padding_rate", "PackMambaError", "load", "F32", "BF16",
     "STATE_STRIDE", "BF16_F32OUT",
@@ -153,6 +154,13 @@ def saved_states_size(batch: int, dim: int, seqlen: int, dstate: int = 16) -> in
     return int(load().packmamba_selective_scan_fwd_saved_states_size(batch, dim, seqlen, dstate))
 
 
+def chunk_states(saved_states, batch: int, dim: int, seqlen: int, dstate: int = 16):
+    """The chunk states inside a saved-states buffer: (batch, dim, chunk, dstate), h after
+    token min((c+1) STATE_STRIDE, seqlen) - 1 of chunk c."""
+    nch = (seqlen + STATE_STRIDE - 1) // STATE_STRIDE
+    return saved_states[:batch * dim * nch * dstate].view(batch, dim, nch, dstate)
+
+
 def selective_scan_fwd(u, delta, A, B, C, D, z, delta_bias, delta_softplus, position_indices,
                        return_states: bool = False, out=True, out_f32: bool = False, workspace=None,
                        initial_state=None, return_final: bool = False):
@@ -168,8 +176,8 @@ def selective_scan_fwd(u, delta, A, B, C, D, z, delta_bias, delta_softplus, posi
     ws = workspace if workspace is not None or need == 0 else _workspace(need, u.device)
     states = None
     if return_states:
-        nch = (L + STATE_STRIDE - 1) // STATE_STRIDE
-        states = torch.empty((Nb, Dn, nch, N), dtype=torch.float32, device=u.device)
+        nbytes = int(lib.packmamba_selective_scan_fwd_saved_states_size(Nb, Dn, L, N))
+        states = torch.empty(nbytes // 4, dtype=torch.float32, device=u.device)
     fin = torch.empty((Nb, Dn, N), dtype=torch.float32, device=u.device) if return_final else None
     st = lib.packmamba_selective_scan_fwd(
         _p(u), _p(delta), _p(A), _p(B), _p(C), _p(D), _p(z), _p(delta_bias), int(delta_softplus),

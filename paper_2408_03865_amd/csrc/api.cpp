@@ -59,8 +59,23 @@ void set_seg_ws(pm::ScanArgs& a, char* base, const SegWs& w) {
     a.ws_carry = w.total ? reinterpret_cast<float*>(base + w.agg) : nullptr;
 }
 
-// Backward workspace: dB/dC partials, per-channel partials, recomputed chunk
-// states (used when no saved states are passed), then the segment workspace.
+// Saved states of the forward: the chunk states (batch, dim, chunk, dstate), then the
+// factor of dout in dz, fp32, per (batch, dim) row padded to whole 256-token chunks,
+// each on an aligned boundary.
+struct SavedLayout {
+    size_t states, dzf, total;
+};
+
+SavedLayout saved_layout(int64_t batch, int64_t dim, int64_t seqlen) {
+    SavedLayout s;
+    s.states = align_up(sizeof(float) * (size_t)(batch * dim * state_chunks(seqlen) * kN));
+    s.dzf = align_up(sizeof(float) * (size_t)(batch * dim * pm::dzf_row_len(seqlen)));
+    s.total = s.states + s.dzf;
+    return s;
+}
+
+// Backward workspace: dB/dC partials, per-channel partials, recomputed saved states
+// (used when none are passed), then the segment workspace.
 struct ScanWs {
     size_t part_bc, part_chan, states, total;
     SegWs seg;
@@ -72,7 +87,7 @@ ScanWs scan_ws(int64_t batch, int64_t dim, int64_t seqlen) {
     ScanWs w;
     w.part_bc = align_up(sizeof(float) * (size_t)(batch * groups * 2 * kN * seqlen));
     w.part_chan = align_up(sizeof(float) * (size_t)(batch * nseg * dim * (kN + 2)));
-    w.states = align_up(sizeof(float) * (size_t)(batch * dim * state_chunks(seqlen) * kN));
+    w.states = saved_layout(batch, dim, seqlen).total;
     w.seg = seg_ws(batch, dim, seqlen);
     w.total = w.part_bc + w.part_chan + w.states + w.seg.total;
     return w;
@@ -157,7 +172,7 @@ int packmamba_causal_conv1d_bwd(const void* x, const float* weight, const float*
 size_t packmamba_selective_scan_fwd_saved_states_size(int64_t batch, int64_t dim, int64_t seqlen,
                                                       int32_t dstate) {
     if (check_shape(batch, dim, seqlen) || dstate != kN) return 0;
-    return sizeof(float) * (size_t)(batch * dim * state_chunks(seqlen) * kN);
+    return saved_layout(batch, dim, seqlen).total;
 }
 
 size_t packmamba_selective_scan_fwd_workspace_size(int64_t batch, int64_t dim, int64_t seqlen,
@@ -191,6 +206,9 @@ int packmamba_selective_scan_fwd(const void* u, const void* delta, const float* 
     a.u = u; a.delta = delta; a.A = A; a.B = B; a.C = C; a.D = D; a.z = z;
     a.delta_bias = delta_bias; a.pos = position_indices; a.softplus = delta_softplus ? 1 : 0;
     a.out = out; a.states = saved_states; a.h0 = initial_state; a.hfinal = final_state;
+    if (saved_states && z)
+        a.dzf = reinterpret_cast<float*>(reinterpret_cast<char*>(saved_states) +
+                                         saved_layout(batch, dim, seqlen).states);
     a.batch = batch; a.dim = dim; a.seqlen = seqlen; a.dstate = dstate; a.dtype = dtype;
     return launch_status(pm::launch_scan_fwd(a, (hipStream_t)stream));
 }
@@ -238,11 +256,12 @@ int packmamba_selective_scan_bwd(const void* u, const void* delta, const float* 
     // the forward recompute below and the backward run one after the other on the
     // stream, so they share the segment workspace
     set_seg_ws(a, ws + w.part_bc + w.part_chan + w.states, w.seg);
-    if (saved_states) {
-        a.states = const_cast<float*>(saved_states);
-    } else {
-        // recompute the chunk states with the forward kernel (no output) into the workspace
-        a.states = reinterpret_cast<float*>(ws + w.part_bc + w.part_chan);
+    char* saved = saved_states ? reinterpret_cast<char*>(const_cast<float*>(saved_states))
+                               : ws + w.part_bc + w.part_chan;
+    a.states = reinterpret_cast<float*>(saved);
+    if (z) a.dzf = reinterpret_cast<float*>(saved + saved_layout(batch, dim, seqlen).states);
+    if (!saved_states) {
+        // recompute the saved states with the forward kernel (no output) into the workspace
         a.out = nullptr;
         if (int e = launch_status(pm::launch_scan_fwd(a, s))) return e;
     }

@@ -82,6 +82,9 @@ struct ScanArgs {
     // forward
     void* out;
     float* states;          // (batch, dim, nchunk, dstate); written by fwd, read by bwd
+    float* dzf;             // (batch, dim, seqlen): (y + D u) d(z sigmoid(z))/dz, the factor of
+                            // dout in dz; written by fwd beside the states when z is given,
+                            // read by bwd (required there when z is given)
     // backward
     const void* dout;
     void* du;
@@ -100,6 +103,23 @@ struct ScanArgs {
     int64_t batch, dim, seqlen;
     int32_t dstate, dtype;
 };
+
+// The factor of dout in dz, saved by the scan forward for the backward (fp32): each
+// (batch, channel) row is padded to whole chunks of kDzfChunk = 256 tokens
+// (dzf_row_len), and a chunk is stored as [i][lane][q] for its token 16 lane + 4 i + q.
+// The forward's lane holds 16 consecutive tokens, and its i-th 16-byte store lands
+// beside the other lanes' i-th stores, so every store instruction writes whole
+// 128-byte lines of a row; the backward's 8-token run (lane j of a 128-token chunk)
+// is two such vectors, also whole lines per wave.
+constexpr int64_t kDzfChunk = 256;
+__host__ __device__ constexpr int64_t dzf_row_len(int64_t L) {
+    return (L + kDzfChunk - 1) / kDzfChunk * kDzfChunk;
+}
+// float offset, inside a padded row, of vector i (tokens 4 i .. 4 i + 3) of lane j's
+// 16 tokens in 256-token chunk c
+__host__ __device__ constexpr int64_t dzf_vec(int64_t c, int i, int j) {
+    return c * kDzfChunk + (i * 16 + j) * 4;
+}
 
 // channels reduced on chip per dB/dC partial in the backward
 constexpr int kScanBwdChannels = 16;

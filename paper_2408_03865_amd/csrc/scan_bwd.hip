@@ -12,10 +12,13 @@
 //     the chunk to the right.  Abar_{l+1} of a token whose successor starts a
 //     sequence is 0 (the matching reset, §3.4): it is the very Abar the replay
 //     computed, shifted by one token;
-//  4. accumulate du, ddelta, dz per token, dA per lane, and write the dB, dC
+//  4. accumulate du, ddelta per token, dA per lane, and write the dB, dC
 //     contributions; these are summed over the block's 16 channels in LDS and
 //     written as one partial per block (part_bc), summed over blocks by
 //     scan_bwd_finalize_bc in a fixed order.
+// dz needs y, which the forward has computed already: it saves the factor
+// (y + D u) d(z sigmoid(z))/dz of dout beside the chunk states, and dz is written at
+// the start of each chunk, so the state loop does not rebuild y.
 // Long rows with few channels are split into segments scanned by different blocks
 // (as in the forward): an aggregate pass folds each segment's reverse recurrence
 // into dh_first = Q x + H, where x is dh at the first token of the next segment,
@@ -48,7 +51,6 @@ struct __attribute__((aligned(16))) BwdSmem {
     float xc[kRows][kN];            // dh at the first token of the chunk to the right
     float an[kRows][kN];            // Abar at the first token of the chunk to the right
     float hin[kRows][kN];           // state at the chunk start (saved by the forward)
-    float gz[kThreads][kK];         // per token: dout * d(z sigmoid(z))/dz, for dz at the chunk end
     float dA[kRows][kN];            // per-channel dA accumulators
 };
 
@@ -64,6 +66,7 @@ struct BwdParams {
     const int32_t* pos;
     const void* dout;
     const float* states;
+    const float* dzf;     // (batch, dim, L): factor of dout in dz, saved by the forward
     const float* h0;      // state before each row (batch, dim, kN), or null
     const float* dhfinal; // gradient of the state after each row, or null
     float* dh0;           // gradient of h0, or null
@@ -130,6 +133,7 @@ void scan_bwd_kernel(BwdParams p) {
     TO* dur = static_cast<TO*>(p.du) + rowoff;
     TO* ddr = static_cast<TO*>(p.ddelta) + rowoff;
     TO* dzr = p.dz ? static_cast<TO*>(p.dz) + rowoff : nullptr;
+    const float* fr = p.dzf ? p.dzf + (b * p.dim + d) * dzf_row_len(L) : nullptr;
     const T* Bb = static_cast<const T*>(p.B) + b * kN * L;
     const T* Cb = static_cast<const T*>(p.C) + b * kN * L;
     const int32_t* pr = p.pos + b * L;
@@ -163,11 +167,20 @@ void scan_bwd_kernel(BwdParams p) {
         // this lane's inputs, loaded first in a full chunk so that their latency
         // overlaps the staging below
         RawRun<T, K> wu, wd, wg, wz;
+        f32x4 wf[2];
         if constexpr (FULL) {
             wu = load_raw<T, K>(ur, l0);
             wd = load_raw<T, K>(dr, l0);
             wg = load_raw<T, K>(gr, l0);
             if (zr) wz = load_raw<T, K>(zr, l0);
+        }
+        if (zr) {
+            // this lane's 8 tokens of the dz factor: vectors 2 (j & 1) and 2 (j & 1) + 1 of
+            // the forward's lane 8 (c & 1) + j / 2 in forward chunk c / 2 (padded row, so
+            // whole vectors even past the row end)
+            const int jf = 8 * (int)(c & 1) + (j >> 1), i0 = 2 * (j & 1);
+            wf[0] = *reinterpret_cast<const f32x4*>(fr + dzf_vec(c >> 1, i0, jf));
+            wf[1] = *reinterpret_cast<const f32x4*>(fr + dzf_vec(c >> 1, i0 + 1, jf));
         }
         // ---- stage B, C, the reset mask and the chunk-start states in LDS ----
         for (int idx = tid * PV; idx < kN * kCH; idx += kThreads * PV) {
@@ -193,7 +206,7 @@ void scan_bwd_kernel(BwdParams p) {
         __syncthreads();
 
         // ---- per-token inputs ----
-        float dt[K], dlu[K], dyD[K], yacc[K], sdhB[K], sdA[K];
+        float dt[K], dlu[K], dyD[K], sdhB[K], sdA[K];
         float S = 0.0f, Mf = 0.0f, Mr = 0.0f, m0 = 0.0f;
         {
             float dl[K], uv[K];
@@ -207,17 +220,18 @@ void scan_bwd_kernel(BwdParams p) {
                 load_run<T, K, FULL>(gr, l0, L, p.vec, dyD);
             }
             if (zr) {
-                float zv[K], gz[K];
+                // dz = dout (y + D u) d(z sigmoid(z))/dz: the forward saved every factor
+                // but dout, so dz is final here; dy = dout SiLU(z) enters the recurrence
+                float zv[K];
                 if constexpr (FULL) unpack_run(wz, zv);
                 else load_run<T, K, FULL>(zr, l0, L, p.vec, zv);
+                float fz[K] = {wf[0].x, wf[0].y, wf[0].z, wf[0].w, wf[1].x, wf[1].y, wf[1].z, wf[1].w};
 #pragma unroll
                 for (int k = 0; k < K; ++k) {
-                    const float sz = sigmoid_f(zv[k]);
-                    gz[k] = dyD[k] * sz * (1.0f + zv[k] * (1.0f - sz));    // dz = gz * (y + D u)
-                    dyD[k] *= zv[k] * sz;                                 // dy = dout * SiLU(z)
+                    fz[k] *= dyD[k];
+                    dyD[k] *= zv[k] * sigmoid_f(zv[k]);
                 }
-                *reinterpret_cast<f32x4*>(&sm.gz[tid][0]) = f32x4{gz[0], gz[1], gz[2], gz[3]};
-                *reinterpret_cast<f32x4*>(&sm.gz[tid][4]) = f32x4{gz[4], gz[5], gz[6], gz[7]};
+                if (active) store_run<TO, K, FULL>(dzr, l0, L, p.vec, fz);
             }
 #pragma unroll
             for (int k = 0; k < K; ++k) {
@@ -228,7 +242,6 @@ void scan_bwd_kernel(BwdParams p) {
                 dt[k] = v;
                 if (!active) dyD[k] = 0.0f;           // padding rows contribute nothing to dB, dC
                 dlu[k] = active ? v * uv[k] : 0.0f;
-                yacc[k] = Dd * uv[k];
                 dDacc = fmaf(dyD[k], uv[k], dDacc);
                 sdhB[k] = 0.0f;
                 sdA[k] = 0.0f;
@@ -311,18 +324,11 @@ void scan_bwd_kernel(BwdParams p) {
             const float hend = fmaf(P, hin, H);
             float hprev = dpp<kRowShr1>(hin, hend);
 #pragma unroll
-            for (int k = 0; k < K; k += 4) {
-                const f32x4 cv = *reinterpret_cast<const f32x4*>(&sm.C[n][j][k]);
-                const float cc[4] = {cv.x, cv.y, cv.z, cv.w};
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const int kk = k + q;
-                    ah[kk] = a[kk] * hprev;
-                    const float h = ah[kk] + bx[kk];
-                    yacc[kk] = fmaf(cc[q], h, yacc[kk]);
-                    bx[kk] = dyD[kk] * h;                    // dC contribution (reuses bx)
-                    hprev = h;
-                }
+            for (int k = 0; k < K; ++k) {
+                ah[k] = a[k] * hprev;
+                const float h = ah[k] + bx[k];
+                bx[k] = dyD[k] * h;                          // dC contribution (reuses bx)
+                hprev = h;
             }
             // ---- reverse recurrence, entering with the carry from the right ----
             const float alast = dpp<kRowShl1>(an, a[0]);        // Abar of the next lane's first token
@@ -391,22 +397,13 @@ void scan_bwd_kernel(BwdParams p) {
                 o_du[k] = fmaf(dyD[k], Dd, dt[k] * sdhB[k]);
                 const float ddt = fmaf(uv[k], sdhB[k], sdA[k] * kLn2);   // sdA was built with A*log2e
                 const float s = dl[k] + dbias;
-                o_dd[k] = ddt * (p.softplus ? (s > 20.0f ? 1.0f : sigmoid_f(s)) : 1.0f);
+                o_dd[k] = p.softplus ? ddt * softplus_grad_f(s, dt[k]) : ddt;
                 dbacc += (FULL || l0 + k < L) ? o_dd[k] : 0.0f;
             }
         }
         if (active) {
             store_run<TO, K, FULL>(dur, l0, L, p.vec, o_du);
             store_run<TO, K, FULL>(ddr, l0, L, p.vec, o_dd);
-            if (dzr) {
-                float o_dz[K];
-                const f32x4 g0 = *reinterpret_cast<const f32x4*>(&sm.gz[tid][0]);
-                const f32x4 g1 = *reinterpret_cast<const f32x4*>(&sm.gz[tid][4]);
-                const float gz[K] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
-#pragma unroll
-                for (int k = 0; k < K; ++k) o_dz[k] = gz[k] * yacc[k];
-                store_run<TO, K, FULL>(dzr, l0, L, p.vec, o_dz);
-            }
         }
         __syncthreads();     // LDS is restaged for the next chunk
     };
@@ -653,9 +650,12 @@ __global__ void scan_bwd_finalize_chan(const float* __restrict__ part, float* __
 
 template <typename T, typename TO>
 hipError_t launch_t(const ScanArgs& a, hipStream_t s) {
+    static_assert(kK == 8 && 2 * kCH == kDzfChunk, "the dz factor layout follows the forward's chunk");
     BwdParams p;
     p.u = a.u; p.delta = a.delta; p.A = a.A; p.B = a.B; p.C = a.C; p.D = a.D; p.z = a.z;
     p.delta_bias = a.delta_bias; p.pos = a.pos; p.dout = a.dout; p.states = a.states;
+    p.dzf = a.z ? a.dzf : nullptr;
+    if (a.z && !a.dzf) return hipErrorInvalidValue;
     p.h0 = a.h0; p.dhfinal = a.dhfinal; p.dh0 = a.dh0;
     p.du = a.du; p.ddelta = a.ddelta; p.dz = a.dz; p.part_bc = a.part_bc; p.part_chan = a.part_chan;
     p.dim = a.dim; p.L = a.seqlen;

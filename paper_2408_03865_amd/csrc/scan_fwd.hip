@@ -19,6 +19,9 @@
 //    a product range that contains a start is therefore 0 inside the fold and the
 //    scan alike (§3.4).
 //  - Tokens past the row end get dt = 0 and u = 0, i.e. the identity (1, 0).
+//  - When the states are saved for the backward and z is given, the kernel also
+//    writes the factor (y + D u) d(z sigmoid(z))/dz of dout in dz (fp32), so that
+//    the backward does not rebuild y.
 //  - Long rows with few channels are split into segments scanned by different
 //    blocks: an aggregate pass folds each segment into one map h -> P h + H per
 //    (channel, state), a carry pass chains the maps along the row, and the main
@@ -59,6 +62,7 @@ struct FwdParams {
     const int32_t* pos;
     void* out;
     float* states;
+    float* dzf;               // (batch, dim, L): factor of dout in dz, or null
     const float* h0;          // state before each row (batch, dim, kN), or null
     float* hfinal;            // state after each row (batch, dim, kN), or null
     float* agg;               // aggregate pass output: (batch, dim, nseg, kN, 2) = (P, H)
@@ -234,15 +238,27 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_kernel(FwdParams p) {
             }
         }
 
-        // ---- gate and store ----
-        if (!AGG && orow && active) {
+        // ---- gate and store; for the backward, the factor of dout in dz ----
+        if (!AGG && active && (orow || p.dzf)) {
             if (zr) {
-                float zv[K];
+                float zv[K], g[K];
                 load_run<T, K, FULL>(zr, l0, L, p.vec, zv);
 #pragma unroll
-                for (int k = 0; k < K; ++k) y[k] = y[k] * zv[k] * sigmoid_f(zv[k]);
+                for (int k = 0; k < K; ++k) {
+                    const float sz = sigmoid_f(zv[k]);
+                    g[k] = y[k] * sz * (1.0f + zv[k] * (1.0f - sz));   // y d(z sigmoid(z))/dz
+                    y[k] = y[k] * zv[k] * sz;
+                }
+                if (p.dzf) {
+                    // padded row: whole vectors, also in a chunk that crosses the row end
+                    float* fr = p.dzf + (b * p.dim + d) * dzf_row_len(L);
+#pragma unroll
+                    for (int i = 0; i < K / 4; ++i)
+                        __builtin_nontemporal_store(f32x4{g[4 * i], g[4 * i + 1], g[4 * i + 2], g[4 * i + 3]},
+                                                    reinterpret_cast<f32x4*>(fr + dzf_vec(c, i, j)));
+                }
             }
-            store_run<TO, K, FULL>(orow, l0, L, p.vec, y);
+            if (orow) store_run<TO, K, FULL>(orow, l0, L, p.vec, y);
         }
         __syncthreads();      // LDS is restaged for the next chunk
     };
@@ -300,9 +316,11 @@ __global__ void scan_fwd_carry_kernel(const float* __restrict__ agg, float* __re
 
 template <typename T, typename TO, int K>
 hipError_t launch_t(const ScanArgs& a, hipStream_t s) {
+    static_assert(16 * K == kDzfChunk && K == 16, "the dz factor layout follows the forward's chunk");
     FwdParams p;
     p.u = a.u; p.delta = a.delta; p.A = a.A; p.B = a.B; p.C = a.C; p.D = a.D; p.z = a.z;
     p.delta_bias = a.delta_bias; p.pos = a.pos; p.out = a.out; p.states = a.states;
+    p.dzf = a.z ? a.dzf : nullptr;
     p.h0 = a.h0; p.hfinal = a.hfinal;
     p.dim = a.dim; p.L = a.seqlen;
     p.nchunk_states = (int)((a.seqlen + kStride - 1) / kStride);

@@ -26,7 +26,7 @@ def test_exports_every_declared_symbol():
     lib = _lib()
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.packmamba_abi_version() == 4
+    assert lib.packmamba_abi_version() == 5
 
 
 def test_status_strings():
@@ -38,8 +38,10 @@ def test_status_strings():
 
 def test_sizes():
     lib = _lib()
-    assert lib.packmamba_selective_scan_fwd_saved_states_size(8, 4096, 4096, 16) == 8 * 4096 * 32 * 16 * 4
-    assert lib.packmamba_selective_scan_fwd_saved_states_size(1, 1, 129, 16) == 2 * 16 * 4
+    # chunk states, then the dz factor (rows padded to 256 tokens) from the next multiple of 256 bytes
+    assert lib.packmamba_selective_scan_fwd_saved_states_size(8, 4096, 4096, 16) == \
+        8 * 4096 * 32 * 16 * 4 + 8 * 4096 * 4096 * 4
+    assert lib.packmamba_selective_scan_fwd_saved_states_size(1, 1, 129, 16) == 256 + 1024   # row padded to 256 tokens
     assert lib.packmamba_selective_scan_fwd_saved_states_size(1, 1, 129, 8) == 0
     assert lib.packmamba_causal_conv1d_bwd_workspace_size(2, 3, 5, 4) >= 2 * 3 * 5 * 4
     assert lib.packmamba_causal_conv1d_bwd_workspace_size(2, 3, 5, 5) == 0
