@@ -42,7 +42,8 @@ constexpr int kWaves = kThreads / 64;
 constexpr int kSeg = kK + 4;        // padded lane segment: conflict-free 16-byte LDS reads
 
 struct __attribute__((aligned(16))) BwdSmem {
-    float red[2][kWaves][2][kCH];   // [state parity][wave][dB|dC][token]: per-wave channel sums
+    float red[2][kWaves][2][2][kCH];   // [state parity][wave][row pair][dB|dC][token]: sums of
+                                       // two channels
                                     // (first: its addresses need no constant offset)
     float B[kN][16][kSeg];          // [state][lane][token]
     float C[kN][16][kSeg];
@@ -271,10 +272,10 @@ void scan_bwd_kernel(BwdParams p) {
         // per-thread LDS addresses of the dB/dC sums and the offset of this thread's
         // partial (token red_t of dB or dC) inside the block's state-0 partials
         const int wr = r & 3;                        // row inside the wave
-        float* const red_w = &sm.red[0][tid >> 6][wr >> 1][j * K + (K / 2) * (wr & 1)];
+        float* const red_w = &sm.red[0][tid >> 6][wr & 1][wr >> 1][j * K];
         const int red_which = __builtin_amdgcn_readfirstlane(tid >> 7);   // 0: dB, 1: dC (per wave)
         const int red_t = tid & (kCH - 1);
-        const float* const red_r = &sm.red[0][0][red_which][red_t];
+        const float* const red_r = &sm.red[0][0][0][red_which][red_t];
         float* const part_n = p.part_bc + ((b * p.groups + g) * 2 + red_which) * kN * L;
         const uint32_t part_off = (uint32_t)(lb + red_t);
 #pragma unroll 1
@@ -354,10 +355,11 @@ void scan_bwd_kernel(BwdParams p) {
             dAl = row_sum_to_15(dAl);
             if (j == 15) sm.dA[r][n] += dAl;
             // ---- dB, dC: sum over the block's 16 channels ----
-            // First over the wave's 4 rows (channels) in registers, by a transposed
-            // butterfly: permlane32_swap pairs rows {0,1} with {2,3} and leaves dB sums
-            // on rows 0-1 and dC sums on rows 2-3; permlane16_swap pairs even with odd
-            // rows and leaves token slots 0-3 on even rows and 4-7 on odd rows.
+            // First over pairs of the wave's 4 rows (channels) in registers:
+            // permlane32_swap pairs rows {0,1} with {2,3} and leaves dB sums on rows 0-1
+            // and dC sums on rows 2-3 (one swap and one add per pair of values; a second
+            // swap stage over even and odd rows measured slower than summing eight
+            // partials instead of four from LDS).
             float R[K];
 #pragma unroll
             for (int k = 0; k < K; ++k) {
@@ -365,21 +367,15 @@ void scan_bwd_kernel(BwdParams p) {
                                                                  __float_as_uint(bx[k]), false, false);
                 R[k] = __uint_as_float(s2[0]) + __uint_as_float(s2[1]);
             }
-            float Q[K / 2];
-#pragma unroll
-            for (int k = 0; k < K / 2; ++k) {
-                const auto s2 = __builtin_amdgcn_permlane16_swap(__float_as_uint(R[k]),
-                                                                 __float_as_uint(R[k + K / 2]), false, false);
-                Q[k] = __uint_as_float(s2[0]) + __uint_as_float(s2[1]);
-            }
-            const int par = (n & 1) * (kWaves * 2 * kCH);
-            *reinterpret_cast<f32x4*>(red_w + par) = f32x4{Q[0], Q[1], Q[2], Q[3]};
+            const int par = (n & 1) * (kWaves * 4 * kCH);
+            *reinterpret_cast<f32x4*>(red_w + par) = f32x4{R[0], R[1], R[2], R[3]};
+            *reinterpret_cast<f32x4*>(red_w + par + 4) = f32x4{R[4], R[5], R[6], R[7]};
             __syncthreads();
             __builtin_amdgcn_s_setprio(0);
-            {   // then over the block's 4 waves, in a fixed order
+            {   // then over the block's 4 waves x 2 row pairs, in a fixed order
                 float s = 0.0f;
 #pragma unroll
-                for (int q = 0; q < kWaves; ++q) s += red_r[par + q * 2 * kCH];
+                for (int q = 0; q < 2 * kWaves; ++q) s += red_r[par + q * 2 * kCH];
                 if (FULL || lb + red_t < L) __builtin_nontemporal_store(s, &part_n[n * L + part_off]);   // read once, by the finalize
             }
             // no second barrier: the next state writes the other buffer, and this one is
