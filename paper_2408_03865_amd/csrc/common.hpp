@@ -104,6 +104,17 @@ __device__ __forceinline__ RawRun<T, K> load_raw(const T* __restrict__ row, int6
     for (int i = 0; i < K / PV; ++i) r.w[i] = *reinterpret_cast<const u32x4*>(row + l0 + i * PV);
     return r;
 }
+// The same, non-temporal: for inputs read once, so that they do not take cache space
+// from inputs that are read again.
+template <typename T, int K>
+__device__ __forceinline__ RawRun<T, K> load_raw_nt(const T* __restrict__ row, int64_t l0) {
+    constexpr int PV = Storage<T>::kPerVec;
+    RawRun<T, K> r;
+#pragma unroll
+    for (int i = 0; i < K / PV; ++i)
+        r.w[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(row + l0 + i * PV));
+    return r;
+}
 template <typename T, int K>
 __device__ __forceinline__ void unpack_run(const RawRun<T, K>& r, float* v) {
     constexpr int PV = Storage<T>::kPerVec;

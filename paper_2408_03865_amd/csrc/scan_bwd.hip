@@ -166,22 +166,23 @@ void scan_bwd_kernel(BwdParams p) {
         const int64_t lb = c * kCH;
         const int64_t l0 = lb + (int64_t)j * K;
         // this lane's inputs, loaded first in a full chunk so that their latency
-        // overlaps the staging below
+        // overlaps the staging below; dout, z and the dz factor are read once
+        // (non-temporal), u and delta again at the chunk end
         RawRun<T, K> wu, wd, wg, wz;
         f32x4 wf[2];
         if constexpr (FULL) {
             wu = load_raw<T, K>(ur, l0);
             wd = load_raw<T, K>(dr, l0);
-            wg = load_raw<T, K>(gr, l0);
-            if (zr) wz = load_raw<T, K>(zr, l0);
+            wg = load_raw_nt<T, K>(gr, l0);
+            if (zr) wz = load_raw_nt<T, K>(zr, l0);
         }
         if (zr) {
             // this lane's 8 tokens of the dz factor: vectors 2 (j & 1) and 2 (j & 1) + 1 of
             // the forward's lane 8 (c & 1) + j / 2 in forward chunk c / 2 (padded row, so
             // whole vectors even past the row end)
             const int jf = 8 * (int)(c & 1) + (j >> 1), i0 = 2 * (j & 1);
-            wf[0] = *reinterpret_cast<const f32x4*>(fr + dzf_vec(c >> 1, i0, jf));
-            wf[1] = *reinterpret_cast<const f32x4*>(fr + dzf_vec(c >> 1, i0 + 1, jf));
+            wf[0] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(fr + dzf_vec(c >> 1, i0, jf)));
+            wf[1] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(fr + dzf_vec(c >> 1, i0 + 1, jf)));
         }
         // ---- stage B, C, the reset mask and the chunk-start states in LDS ----
         for (int idx = tid * PV; idx < kN * kCH; idx += kThreads * PV) {
