@@ -203,10 +203,12 @@ def cold_steps(step_fn, stream, steps, flush_bytes=1 << 29):
             "steps": steps}
 
 
-def with_states(lib, tens, pos_host, code, width, stream, steps, warmup, packed_ms):
+def with_states(lib, tens, pos_host, code, width, stream, steps, warmup, packed_step):
     """The same step with every row continuing a sequence cut at the end of another row
     (its first sequence's position indices start at 100), initial states in, final
-    states out, and their gradients: the state-passing path."""
+    states out, and their gradients: the state-passing path.  Timed alternately with
+    the packed step (three rounds each, medians), so that both see the same memory and
+    cache conditions."""
     import numpy as np
     import torch
     pos = pos_host.copy()
@@ -217,9 +219,13 @@ def with_states(lib, tens, pos_host, code, width, stream, steps, warmup, packed_
     t = dict(tens, pos=torch.from_numpy(pos).to(tens["x"].device))
     ch = Chain(lib, t, code, width, stream, states=True)
     ops = [f for _, f in ch.ops()]
-    ms = time_steps(lambda: [f() for f in ops], stream, steps, warmup)
-    return {"ms_per_step": round(ms, 4), "overhead_vs_packed": round(ms / packed_ms - 1.0, 4),
-            "rows_continued": int(pos.shape[0])}
+    packed, cont = [], []
+    for _ in range(3):
+        packed.append(time_steps(packed_step, stream, steps, warmup))
+        cont.append(time_steps(lambda: [f() for f in ops], stream, steps, warmup))
+    ms, ref = float(np.median(cont)), float(np.median(packed))
+    return {"ms_per_step": round(ms, 4), "packed_ms_per_step": round(ref, 4),
+            "overhead_vs_packed": round(ms / ref - 1.0, 4), "rows_continued": int(pos.shape[0])}
 
 
 def packing_rates(law, seqlen, count=20000, seed=0):
@@ -548,8 +554,8 @@ def main():
     }
     if args.config == "2" and not args.no_compare:
         print("# state passing: every row continues a sequence", file=sys.stderr, flush=True)
-        line["state_passing"] = with_states(lib, tens, d["pos"], code, Wd, stream, steps=10, warmup=2,
-                                            packed_ms=ms_step)
+        line["state_passing"] = with_states(lib, tens, d["pos"], code, Wd, stream, steps=10, warmup=3,
+                                            packed_step=step)
         print("# comparison: padded and single-sequence runs of the same tokens", file=sys.stderr, flush=True)
         line["comparison"] = comparison(lib, tens, d["pos"], code, Wd, stream, steps=5, warmup=2,
                                         packed_ms=ms_step)

@@ -127,9 +127,10 @@ __device__ __forceinline__ void unpack_run(const RawRun<T, K>& r, float* v) {
 // consecutive bytes, and the store is non-temporal: every output here is streamed
 // out once, and keeping it out of the caches leaves them to the inputs that are read
 // again.  With more vectors per lane each store covers every other 16 bytes of its
-// range; such partial lines are left to the caches to combine (no gain was measured
-// from making them non-temporal).
-template <typename T, int K, bool FULL = false>
+// range; such partial lines are left to the caches to combine unless NT says
+// otherwise (non-temporal, the fp32 conv backward's dx ran 40% slower, while the fp32
+// scan backward's outputs gained 2%).
+template <typename T, int K, bool FULL = false, bool NT = (K == Storage<T>::kPerVec)>
 __device__ __forceinline__ void store_run(T* __restrict__ row, int64_t l0, int64_t L, bool vec,
                                           const float* v) {
     constexpr int PV = Storage<T>::kPerVec;
@@ -137,7 +138,7 @@ __device__ __forceinline__ void store_run(T* __restrict__ row, int64_t l0, int64
 #pragma unroll
         for (int i = 0; i < K / PV; ++i) {
             u32x4* dst = reinterpret_cast<u32x4*>(row + l0 + i * PV);
-            if constexpr (K == PV) __builtin_nontemporal_store(Storage<T>::pack(v + i * PV), dst);
+            if constexpr (NT) __builtin_nontemporal_store(Storage<T>::pack(v + i * PV), dst);
             else *dst = Storage<T>::pack(v + i * PV);
         }
     } else {

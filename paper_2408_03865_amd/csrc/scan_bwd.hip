@@ -233,7 +233,7 @@ void scan_bwd_kernel(BwdParams p) {
                     fz[k] *= dyD[k];
                     dyD[k] *= zv[k] * sigmoid_f(zv[k]);
                 }
-                if (active) store_run<TO, K, FULL>(dzr, l0, L, p.vec, fz);
+                if (active) store_run<TO, K, FULL, true>(dzr, l0, L, p.vec, fz);
             }
 #pragma unroll
             for (int k = 0; k < K; ++k) {
@@ -399,8 +399,8 @@ void scan_bwd_kernel(BwdParams p) {
             }
         }
         if (active) {
-            store_run<TO, K, FULL>(dur, l0, L, p.vec, o_du);
-            store_run<TO, K, FULL>(ddr, l0, L, p.vec, o_dd);
+            store_run<TO, K, FULL, true>(dur, l0, L, p.vec, o_du);
+            store_run<TO, K, FULL, true>(ddr, l0, L, p.vec, o_dd);
         }
         __syncthreads();     // LDS is restaged for the next chunk
     };
