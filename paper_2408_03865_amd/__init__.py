@@ -138,14 +138,16 @@ def rmsnorm_bwd(x, weight, rstd, dout, dresidual=None, workspace=None, out_f32: 
     return dx, dw
 
 
-def segments(batch: int, dim: int, seqlen: int) -> int:
-    """Segments per row the scans use for this shape (1: rows are not split).  Mirrors
-    the rule of the library's launchers, for tests and reports only."""
+def segments(batch: int, dim: int, seqlen: int, direction: str = "bwd") -> int:
+    """Segments per row the scan forward ("fwd") or backward ("bwd") uses for this shape
+    (1: rows are not split).  Mirrors the rule of the library's launchers, for tests and
+    reports only."""
+    target = {"fwd": 768, "bwd": 1536}[direction]
     blocks = batch * ((dim + 15) // 16)
     units = (seqlen + 255) // 256
-    if blocks * 2 >= 1536 or units < 2:
+    if blocks * 2 >= target or units < 2:
         return 1
-    nseg = min((1536 + blocks - 1) // blocks, units)
+    nseg = min((target + blocks - 1) // blocks, units)
     per = (units + nseg - 1) // nseg
     return (units + per - 1) // per
 

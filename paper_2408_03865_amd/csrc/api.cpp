@@ -43,8 +43,8 @@ struct SegWs {
     size_t agg, carry, total;
 };
 
-SegWs seg_ws(int64_t batch, int64_t dim, int64_t seqlen) {
-    const pm::SegPlan sp = pm::scan_segments(batch, dim, seqlen);
+SegWs seg_ws(int64_t batch, int64_t dim, int64_t seqlen, int64_t target) {
+    const pm::SegPlan sp = pm::scan_segments(batch, dim, seqlen, target);
     SegWs w{0, 0, 0};
     if (sp.nseg > 1) {
         w.agg = align_up(sizeof(float) * (size_t)(batch * dim * sp.nseg * kN * 2));
@@ -83,12 +83,12 @@ struct ScanWs {
 
 ScanWs scan_ws(int64_t batch, int64_t dim, int64_t seqlen) {
     const int64_t groups = (dim + pm::kScanBwdChannels - 1) / pm::kScanBwdChannels;
-    const int64_t nseg = pm::scan_segments(batch, dim, seqlen).nseg;
+    const int64_t nseg = pm::scan_segments(batch, dim, seqlen, pm::kSegTargetBwd).nseg;
     ScanWs w;
     w.part_bc = align_up(sizeof(float) * (size_t)(batch * groups * 2 * kN * seqlen));
     w.part_chan = align_up(sizeof(float) * (size_t)(batch * nseg * dim * (kN + 2)));
     w.states = saved_layout(batch, dim, seqlen).total;
-    w.seg = seg_ws(batch, dim, seqlen);
+    w.seg = seg_ws(batch, dim, seqlen, pm::kSegTargetBwd);   // covers the forward's plan too
     w.total = w.part_bc + w.part_chan + w.states + w.seg.total;
     return w;
 }
@@ -178,7 +178,7 @@ size_t packmamba_selective_scan_fwd_saved_states_size(int64_t batch, int64_t dim
 size_t packmamba_selective_scan_fwd_workspace_size(int64_t batch, int64_t dim, int64_t seqlen,
                                                    int32_t dstate) {
     if (check_shape(batch, dim, seqlen) || dstate != kN) return 0;
-    return seg_ws(batch, dim, seqlen).total;
+    return seg_ws(batch, dim, seqlen, pm::kSegTargetFwd).total;
 }
 
 int packmamba_selective_scan_fwd(const void* u, const void* delta, const float* A, const void* B,
@@ -199,7 +199,7 @@ int packmamba_selective_scan_fwd(const void* u, const void* delta, const float* 
         !aligned16(position_indices) || !aligned16(out) || !aligned16(saved_states) ||
         !aligned16(workspace) || !aligned16(initial_state) || !aligned16(final_state))
         return PACKMAMBA_ERR_ALIGN;
-    const SegWs w = seg_ws(batch, dim, seqlen);
+    const SegWs w = seg_ws(batch, dim, seqlen, pm::kSegTargetFwd);
     if (w.total && (!workspace || workspace_bytes < w.total)) return PACKMAMBA_ERR_WORKSPACE;
     pm::ScanArgs a{};
     set_seg_ws(a, static_cast<char*>(workspace), w);

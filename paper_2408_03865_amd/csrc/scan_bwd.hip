@@ -660,7 +660,7 @@ hipError_t launch_t(const ScanArgs& a, hipStream_t s) {
     p.groups = (int)((a.dim + kRows - 1) / kRows);
     p.softplus = a.softplus;
     p.vec = (a.seqlen % Storage<T>::kPerVec) == 0 && (a.seqlen % Storage<TO>::kPerVec) == 0;
-    const SegPlan sp = scan_segments(a.batch, a.dim, a.seqlen);
+    const SegPlan sp = scan_segments(a.batch, a.dim, a.seqlen, kSegTargetBwd);
     static_assert(kSegUnit % kCH == 0, "segments hold whole chunks");
     p.seg_chunks = sp.seg_len / kCH;
     p.nseg = (int)sp.nseg;

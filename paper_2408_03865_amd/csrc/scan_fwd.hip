@@ -326,7 +326,7 @@ hipError_t launch_t(const ScanArgs& a, hipStream_t s) {
     p.nchunk_states = (int)((a.seqlen + kStride - 1) / kStride);
     p.softplus = a.softplus;
     p.vec = (a.seqlen % Storage<T>::kPerVec) == 0 && (a.seqlen % Storage<TO>::kPerVec) == 0;
-    const SegPlan sp = scan_segments(a.batch, a.dim, a.seqlen);
+    const SegPlan sp = scan_segments(a.batch, a.dim, a.seqlen, kSegTargetFwd);
     static_assert(kSegUnit % (16 * K) == 0, "segments hold whole chunks");
     p.seg_chunks = sp.seg_len / (16 * K);
     p.nseg = (int)sp.nseg;

@@ -50,7 +50,7 @@ def test_sizes():
     # forward workspace: only for shapes whose rows are split into segments
     assert lib.packmamba_selective_scan_fwd_workspace_size(8, 4096, 4096, 16) == 0
     assert lib.packmamba_selective_scan_fwd_workspace_size(1, 2048, 256, 16) == 0      # one 256-token unit
-    assert lib.packmamba_selective_scan_fwd_workspace_size(1, 2048, 65536, 16) >= 1 * 2048 * 12 * 16 * 12
+    assert lib.packmamba_selective_scan_fwd_workspace_size(1, 2048, 65536, 16) >= 1 * 2048 * 6 * 16 * 12   # 6 segments
     assert lib.packmamba_selective_scan_fwd_workspace_size(0, 2048, 65536, 16) == 0
     assert (lib.packmamba_selective_scan_bwd_workspace_size(1, 2048, 65536, 16)
             > lib.packmamba_selective_scan_fwd_workspace_size(1, 2048, 65536, 16))
@@ -62,17 +62,23 @@ def test_segment_rule():
     import paper_2408_03865_amd as P
     lib = _lib()
     for shape in [(8, 4096, 4096), (8, 5120, 4096), (4, 1536, 2048), (2, 2048, 8192), (1, 2048, 65536),
-                  (1, 64, 256), (1, 64, 257), (1, 16, 100000), (3, 700, 3000), (47, 16, 512)]:
-        ns = P.segments(*shape)
+                  (1, 64, 256), (1, 64, 257), (1, 16, 100000), (3, 700, 3000), (47, 16, 512),
+                  (24, 16, 4096), (40, 16, 4096)]:
+        b, d, _ = shape
+        nf, nb = P.segments(*shape, direction="fwd"), P.segments(*shape)
+        assert nf <= nb, shape                      # the backward's workspace covers the forward's plan
         ws = lib.packmamba_selective_scan_fwd_workspace_size(*shape, 16)
-        assert (ns > 1) == (ws > 0), shape
-        if ns > 1:
-            b, d, _ = shape
-            assert ws >= b * d * ns * 16 * 12, shape
+        assert (nf > 1) == (ws > 0), shape
+        if nf > 1:
+            assert ws >= b * d * nf * 16 * 12, shape
+        wsb = lib.packmamba_selective_scan_bwd_workspace_size(*shape, 16)
+        if nb > 1:
+            assert wsb >= b * d * nb * 16 * 12, shape
     assert P.segments(8, 4096, 4096) == 1
-    assert P.segments(1, 2048, 65536) == 12
-    assert P.segments(2, 2048, 8192) == 6
-    assert P.segments(4, 1536, 2048) == 4
+    assert P.segments(1, 2048, 65536) == 12 and P.segments(1, 2048, 65536, "fwd") == 6
+    assert P.segments(2, 2048, 8192) == 6 and P.segments(2, 2048, 8192, "fwd") == 3
+    assert P.segments(4, 1536, 2048) == 4 and P.segments(4, 1536, 2048, "fwd") == 1   # 384 blocks
+    assert P.segments(500, 16, 4096) == 4 and P.segments(500, 16, 4096, "fwd") == 1   # forward unsplit
 
 
 def _gpu_visible():

@@ -108,6 +108,24 @@ def test_backward_without_saved_states_is_identical():
         assert np.array_equal(host(a[k]), host(b[k])), k
 
 
+@pytest.mark.parametrize("key", ["1", "4a"])
+def test_recompute_with_different_splits_is_identical(key):
+    """Rows split differently by the two directions (config 1: forward unsplit, backward
+    in 4 segments; 4a: 3 and 6): the backward's recompute of the saved states runs the
+    forward's plan inside the backward's segment workspace, and must match the saved
+    path bit for bit."""
+    import paper_2408_03865_amd as P
+    cfg = W.config(key)
+    assert P.segments(cfg.batch, cfg.dim, cfg.seqlen, "fwd") < P.segments(cfg.batch, cfg.dim, cfg.seqlen)
+    note(f"recompute vs saved states, config {key}")
+    d = W.make_inputs(cfg)
+    g = gpu_inputs(d, cfg.dtype)
+    a = run_gpu(g, states=True)
+    b = run_gpu(g, states=False)
+    for k in ("du", "ddelta", "dz", "dA", "dB", "dC", "dD", "ddelta_bias"):
+        assert np.array_equal(host(a[k]), host(b[k])), k
+
+
 def test_deterministic():
     cfg = W.config("1", dim=64, seqlen=1024, batch=2)
     d = W.make_inputs(cfg)
