@@ -166,9 +166,10 @@ def chunk_states(saved_states, batch: int, dim: int, seqlen: int, dstate: int = 
 def selective_scan_fwd(u, delta, A, B, C, D, z, delta_bias, delta_softplus, position_indices,
                        return_states: bool = False, out=True, out_f32: bool = False, workspace=None,
                        initial_state=None, return_final: bool = False):
-    """out, followed by the saved states (return_states) and the final state
-    (return_final, (batch, dim, dstate) fp32) when asked for; initial_state is
-    (batch, dim, dstate) fp32."""
+    """out, followed by the saved states (return_states: a flat fp32 buffer for the
+    backward, holding the chunk states, see chunk_states, and the dz factor) and the
+    final state (return_final, (batch, dim, dstate) fp32) when asked for; initial_state
+    is (batch, dim, dstate) fp32."""
     torch = _torch()
     Nb, Dn, L = u.shape
     N = A.shape[1]
