@@ -59,7 +59,7 @@ def kernel_hash() -> str:
 
 def stored_traffic():
     """HBM traffic of the dominant kernel from the last counter run, if its source is unchanged."""
-    p = os.path.join(ROOT, "profiles", "scan_bwd_traffic.json")
+    p = os.path.join(ROOT, "profiles", "scan_bwd_traffic_mamba1.4b_step.json")
     try:
         with open(p) as fh:
             t = json.load(fh)
