@@ -135,3 +135,25 @@ def test_check_position_indices():
         bad[b, l] = v
         import oracle
         assert P.check_position_indices(i32(bad)) == (oracle.check_positions(bad) == -1), (b, l, v)
+
+
+# Long rows with few channels and long sequences: every row is cut into the most
+# segments its 256-token units allow (hundreds), and the carries of both directions
+# chain through all of them inside a sequence.
+LONG = [(1, 16, 100000), (2, 48, 40000)]
+
+
+@pytest.mark.parametrize("shape", LONG, ids=lambda s: "x".join(map(str, s)))
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_long_rows_many_segments(shape, dtype):
+    import paper_2408_03865_amd as P
+    batch, dim, seqlen = shape
+    nf, nb = P.segments(*shape, direction="fwd"), P.segments(*shape)
+    assert nf >= 64 and nb >= 150, (nf, nb)
+    cfg = W.Config("edge", "edge", batch, seqlen, dim, 16, 4, dtype, ("lognormal", 10.5, 0.3, 1, seqlen),
+                   7700 + batch * 131 + dim)
+    note(f"edge long rows {shape} {dtype}: {nf} forward and {nb} backward segments")
+    d = W.make_inputs(cfg)
+    assert len(d["lengths"]) <= 8 * batch               # sequences of tens of thousands of tokens
+    r = run_gpu(gpu_inputs(d, dtype), out_f32=(dtype == "bf16"))
+    compare(r, oracle_run(d), TOL[dtype], ALL, label=f"{shape} {dtype} ")
