@@ -4,9 +4,9 @@ SiLU(z) gate, output projection, residual -- forward and backward.
 
 The sequence-wise steps (conv, scan) and RMSNorm (with the residual's gradient
 folded into its backward) run in this library's HIP kernels through the C ABI; the
-projections are plain GEMMs, run by hipBLASLt through torch.matmul; the residual add
-of the forward is one torch addition (§3.2: token-wise and element-wise operators
-satisfy PUI unchanged, so packing needs nothing from them).  Activations are
+projections are plain GEMMs, run by hipBLASLt through torch.matmul / baddbmm, which
+also add the residual and accumulate the two-term input gradients (§3.2: token-wise and
+element-wise operators satisfy PUI unchanged, so packing needs nothing from them).  Activations are
 laid out (batch, features, seqlen), sequence innermost, which is the layout of the
 conv and scan kernels, so no transposes sit between the steps: each projection is a
 batched GEMM W @ X[b], split per output part so that every tensor the kernels see is
@@ -43,14 +43,20 @@ def _lin_dx(W, dY):
 
 def _lin_dw(dY, X):
     """dW = sum_b dY[b] @ X[b]^T: one 2-D GEMM per batch row, X[b] read transposed in
-    place (no copy), accumulated in fp32 and returned in dY's dtype."""
+    place (no copy), accumulated in fp32 in place (a new accumulator per row would be
+    copied first) and returned in dY's dtype."""
     torch = _torch()
     f32 = torch.float32
     kw = {} if dY.dtype == f32 else {"out_dtype": f32}
     acc = torch.mm(dY[0], X[0].t(), **kw)
     for b in range(1, dY.shape[0]):
-        acc = torch.addmm(acc, dY[b], X[b].t(), **kw)
+        torch.addmm(acc, dY[b], X[b].t(), out=acc, **kw)
     return acc.to(dY.dtype)
+
+
+def _bcast(W, batch):
+    """W as the batched left operand of a GEMM (stride 0 over the batch)."""
+    return W.contiguous().expand(batch, -1, -1)
 
 
 def block_forward(x, pos, p: Dict[str, object], mark: Optional[Callable[[str], None]] = None):
@@ -76,7 +82,7 @@ def block_forward(x, pos, p: Dict[str, object], mark: Optional[Callable[[str], N
     y, st = P.selective_scan_fwd(u, delta, p["A"], B, C, p["D"], z, p["dt_bias"], True, pos,
                                  return_states=True)
     mk("out_proj")
-    out = x + _lin(p["W_out"], y)
+    out = _torch().baddbmm(x, _bcast(p["W_out"], x.shape[0]), y)    # the residual added by the GEMM
     mk("end")
     ctx = dict(x=x, pos=pos, h=h, r=r, xi=xi, z=z, u=u, dtl=dtl, B=B, C=C, delta=delta, y=y, st=st)
     return out, ctx
@@ -101,15 +107,14 @@ def block_backward(dout, ctx, p, mark: Optional[Callable[[str], None]] = None) -
     ddtl = _lin_dx(p["W_dt"], s["ddelta"])
     dxdbl = _torch().cat([ddtl, s["dB"].to(dt), s["dC"].to(dt)], 1)      # (batch, R + 2N, L)
     g["W_x"] = _lin_dw(dxdbl, ctx["u"])
-    du = _lin_dx(Wx, dxdbl)
-    du += s["du"]
+    du = s["du"].baddbmm_(_bcast(Wx.t(), dxdbl.shape[0]), dxdbl)   # accumulated into the scan's du
     mk("conv_bwd")
     dxi, g["conv_w"], g["conv_b"] = P.causal_conv1d_bwd(ctx["xi"], p["conv_w"], p["conv_b"], ctx["pos"],
                                                         du.contiguous(), silu=True)
     mk("in_proj_bwd")
     g["W_in"] = _torch().cat([_lin_dw(dxi, ctx["h"]), _lin_dw(s["dz"], ctx["h"])], 0)
     dh = _lin_dx(p["W_in"][:Dn], dxi)
-    dh += _lin_dx(p["W_in"][Dn:], s["dz"])
+    dh.baddbmm_(_bcast(p["W_in"][Dn:].t(), dh.shape[0]), s["dz"])
     mk("norm_bwd")
     # the residual's gradient (dout itself) is added inside the RMSNorm backward
     g["x"], g["norm_w"] = P.rmsnorm_bwd(ctx["x"], p["norm_w"], ctx["r"], dh, dresidual=dout)

@@ -288,7 +288,7 @@ int packmamba_rmsnorm_fwd(const void* x, const float* weight, float eps, void* o
 size_t packmamba_rmsnorm_bwd_workspace_size(int64_t batch, int64_t dim, int64_t seqlen) {
     if (check_shape(batch, dim, seqlen)) return 0;
     const int64_t tiles = (seqlen + pm::kRmsTile - 1) / pm::kRmsTile;
-    return align_up(sizeof(float) * (size_t)(batch * tiles * dim));
+    return align_up(sizeof(float) * (size_t)((batch * tiles + pm::kRmsSlabs) * dim));
 }
 
 int packmamba_rmsnorm_bwd(const void* x, const float* weight, const float* rstd, const void* dout,

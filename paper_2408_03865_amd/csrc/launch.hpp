@@ -32,6 +32,7 @@ hipError_t launch_conv1d_bwd(const ConvArgs& a, hipStream_t s);
 
 // RMSNorm over the feature axis of (batch, dim, seqlen) activations.
 constexpr int64_t kRmsTile = 64;     // tokens per block; one dweight partial per (batch, tile)
+constexpr int kRmsSlabs = 16;        // row slabs of the dweight reduction's first pass
 struct RmsArgs {
     const void* x;
     const float* w;
@@ -41,7 +42,7 @@ struct RmsArgs {
     void* out;          // fwd: out; bwd: dx
     float* rstd_out;    // fwd: (batch, seqlen)
     float* dw;          // bwd only
-    float* partial;     // bwd only: (batch, tiles, dim)
+    float* partial;     // bwd only: (batch, tiles, dim), then (kRmsSlabs, dim) slab sums
     float eps;
     int64_t batch, dim, seqlen;
     int32_t dtype;
