@@ -48,15 +48,16 @@ class PackMambaError(RuntimeError):
 
 
 _lib = None
+_lib_path = None   # the file _lib was loaded from
 
 
 def load(path: Optional[str] = None) -> ctypes.CDLL:
     """Load the HIP library (raises if it is absent: build with paper_2408_03865_amd/build.py).
     Without a path, the library named by LIB_PATH when the call is made, loaded once."""
-    global _lib
+    global _lib, _lib_path
     if path is None:
         path = LIB_PATH
-    if _lib is not None and path == LIB_PATH:
+    if _lib is not None and path == _lib_path:
         return _lib
     if not os.path.exists(path):
         raise FileNotFoundError(f"{path} is missing; build it with `python paper_2408_03865_amd/build.py`")
@@ -100,7 +101,7 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     if lib.packmamba_abi_version() != ABI_VERSION:
         raise RuntimeError("libpackmamba ABI version mismatch")
     if path == LIB_PATH:
-        _lib = lib
+        _lib, _lib_path = lib, path
     return lib
 
 

@@ -186,3 +186,22 @@ def test_one_hip_runtime_per_process():
     r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=300)
     assert r.returncode == 0, r.stderr
     assert r.stdout.strip().splitlines()[-1] == "1"
+
+
+def test_load_follows_lib_path(tmp_path):
+    """load() without a path returns the library that LIB_PATH names when it is called,
+    also after LIB_PATH has changed (each file is loaded once)."""
+    import shutil
+    from paper_2408_03865_amd import _lib as L
+    first = _lib()
+    old = L.LIB_PATH
+    copy = tmp_path / "libpackmamba_copy.so"
+    shutil.copy(old, copy)
+    try:
+        L.LIB_PATH = str(copy)
+        second = L.load()
+        assert second._name == str(copy) and second is not first
+        assert L.load() is second
+    finally:
+        L.LIB_PATH = old
+    assert L.load()._name == old
