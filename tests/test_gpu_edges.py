@@ -4,7 +4,7 @@ import numpy as np
 import pytest
 
 import workloads as W
-from gpu_common import PER_B, PER_CHANNEL, PER_TOKEN, TOL, compare, gpu_inputs, i32, note, oracle_run, run_gpu
+from gpu_common import PER_B, PER_CHANNEL, PER_TOKEN, TOL, compare, gpu_inputs, host, i32, note, oracle_run, run_gpu
 
 pytestmark = pytest.mark.gpu
 
@@ -157,3 +157,51 @@ def test_long_rows_many_segments(shape, dtype):
     assert len(d["lengths"]) <= 8 * batch               # sequences of tens of thousands of tokens
     r = run_gpu(gpu_inputs(d, dtype), out_f32=(dtype == "bf16"))
     compare(r, oracle_run(d), TOL[dtype], ALL, label=f"{shape} {dtype} ")
+
+
+# Extreme steps and decays: per channel, s = delta + delta_bias is centred on a level
+# spread over [-40, 40] (softplus is the identity far above its threshold of 20 and
+# e^s ~ 4e-18 at the bottom, where every multiplier rounds to 1), and |A| is
+# log-uniform over [3e-4, 20], so dt A runs from about -1e-21 (multipliers of exactly
+# 1 along whole sequences) to -800 (exp underflows to exactly 0 in both precisions).
+# On an unsplit shape and on a row split into 24 segments in both directions.
+# Steps of 20-40 with slow decays drive the states to ~1e3, so an output or gradient
+# can be a small difference of large fp32 terms: fp32 sums over the 16 states (and
+# the in-chunk and carry recurrences) err by up to a few ulps of the largest term,
+# not of the result.  Each tensor is therefore held to the usual scaled bound plus a
+# normwise floor of 16 * 2^-24 * max|ref| (an ulp of the largest term per summed state).
+EXTREME = [(48, 256, 520), (1, 16, 6000)]
+
+
+def _compare_normwise(gr, ref, tol, label):
+    worst = {}
+    for k in ALL:
+        if ref.get(k) is None:
+            continue
+        got = np.asarray(host(gr[k]), dtype=np.float64)
+        r = np.asarray(ref[k], dtype=np.float64)
+        assert got.shape == r.shape and np.all(np.isfinite(got)), k
+        bound = tol * (1.0 + np.abs(r)) + 16.0 * 2.0 ** -24 * float(np.abs(r).max())
+        ratio = np.abs(got - r) / bound
+        i = np.unravel_index(int(np.argmax(ratio)), ratio.shape)
+        assert ratio[i] <= 1.0, f"{label}{k}: error {abs(got[i] - r[i]):.3e} over bound {bound[i]:.3e} at {i}: got {got[i]!r} ref {r[i]!r}"
+        worst[k] = float(ratio[i])
+    note(f"{label} worst error / bound: " + ", ".join(f"{k}={v:.2e}" for k, v in worst.items()))
+
+
+@pytest.mark.parametrize("shape", EXTREME, ids=lambda s: "x".join(map(str, s)))
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_extreme_steps_and_decays(shape, dtype):
+    batch, dim, seqlen = shape
+    cfg = W.Config("edge", "edge", batch, seqlen, dim, 16, 4, dtype, ("lognormal", 6.0, 1.0, 16, seqlen),
+                   7900 + batch * 131 + dim)
+    note(f"edge extreme steps and decays {shape} {dtype}")
+    d = W.make_inputs(cfg, variant="general")
+    rng = np.random.default_rng(7900 + seqlen)
+    level = rng.permutation(np.linspace(-40.0, 40.0, dim))
+    s = level[None, :, None] + rng.normal(0.0, 1.5, size=d["delta"].shape)
+    delta = (s - d["delta_bias"][None, :, None]).astype(np.float32)
+    d["delta"] = W.bf16_round(delta) if dtype == "bf16" else delta
+    d["A"] = (-np.exp(rng.uniform(np.log(3e-4), np.log(20.0), size=d["A"].shape))).astype(np.float32)
+    r = run_gpu(gpu_inputs(d, dtype), out_f32=(dtype == "bf16"))
+    _compare_normwise(r, oracle_run(d), TOL[dtype], label=f"extreme {shape} {dtype} ")
