@@ -57,15 +57,18 @@ def kernel_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def stored_traffic():
-    """HBM traffic of the dominant kernel from the last counter run, if its source is unchanged."""
+def stored_traffic(shape):
+    """HBM traffic of the dominant kernel from the last counter run, if its source is unchanged
+    and the run measured this shape (batch, seqlen, dim, dstate, storage); else None."""
     p = os.path.join(ROOT, "profiles", "scan_bwd_traffic_mamba1.4b_step.json")
     try:
         with open(p) as fh:
             t = json.load(fh)
     except (OSError, ValueError):
         return None
-    return t if t.get("kernel_hash") == kernel_hash() else None
+    if t.get("kernel_hash") != kernel_hash() or t.get("shape") != shape:
+        return None
+    return t
 
 
 def cpu_baseline(d, cfg, rows):
@@ -500,7 +503,7 @@ def main():
     print(f"# timed {args.steps} steps: {ms_step:.3f} ms/step (wall {t_wall / args.steps * 1e3:.3f})",
           file=sys.stderr, flush=True)
 
-    # ---- per-op durations, HIP events on the launch stream ----
+    # ---- per-op durations: mean launch duration, HIP events on the launch stream ----
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(ops) + 1)] for _ in range(args.steps)]
     for it in range(args.steps):
         evs[it][0].record(stream)
@@ -508,7 +511,7 @@ def main():
             f()
             evs[it][i + 1].record(stream)
     torch.cuda.synchronize()
-    op_ms = {name: float(np.median([evs[it][i].elapsed_time(evs[it][i + 1]) for it in range(args.steps)]))
+    op_ms = {name: float(np.mean([evs[it][i].elapsed_time(evs[it][i + 1]) for it in range(args.steps)]))
              for i, (name, _) in enumerate(ops)}
     cold = cold_steps(step, stream, args.steps)
     cold["tokens_per_s"] = round(Nb * L / (cold["ms_per_step"] * 1e-3), 1)
@@ -521,7 +524,7 @@ def main():
     bwd_s = op_ms["scan_bwd"] * 1e-3
     achieved = E * N * SLOTS_BWD / bwd_s / 1e12
     peak = VALU_PEAK / 1e12
-    traffic = stored_traffic()
+    traffic = stored_traffic({"batch": Nb, "seqlen": L, "dim": Dn, "dstate": N, "storage": cfg.dtype})
     roof = {
         "bound": "alu", "achieved": round(achieved, 3), "peak": round(peak, 3), "unit": "Tslot/s",
         "frac": round(achieved / peak, 4),

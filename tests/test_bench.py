@@ -36,3 +36,14 @@ def test_more_than_one_gpu_is_refused():
                        text=True, env=env, timeout=120)
     assert r.returncode == 2
     assert "one GPU" in r.stderr
+
+
+def test_stored_traffic_only_for_the_measured_shape():
+    """The counter-based traffic is reported only for the shape the counters were taken on
+    (and only while the kernel source is unchanged)."""
+    import bench
+    shape = {"batch": 8, "seqlen": 4096, "dim": 4096, "dstate": 16, "storage": "bf16"}
+    t = bench.stored_traffic(shape)
+    assert t is None or (t["shape"] == shape and t["kernel_hash"] == bench.kernel_hash())
+    for other in ({**shape, "dim": 5120}, {**shape, "storage": "f32"}, {**shape, "batch": 4, "seqlen": 2048}):
+        assert bench.stored_traffic(other) is None
