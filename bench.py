@@ -410,7 +410,9 @@ def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    # 20 warm-up steps by default: the clocks settle only after tens of milliseconds of work
+    # (5 left the short configs' timed steps up to 8% slow)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--config", default="2")
     ap.add_argument("--variant", default="paper", choices=["paper", "general"])
     ap.add_argument("--dtype", default=None, choices=["f32", "bf16"],
@@ -489,30 +491,26 @@ def main():
         step()
     torch.cuda.synchronize()
 
-    # ---- timed region: exactly K steps ----
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # ---- timed region: exactly K steps, with a HIP event on the launch stream after every
+    # op, so that each op's mean launch duration comes from the timed steps themselves ----
+    nops = len(ops)
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps * nops + 1)]
     torch.cuda.synchronize()
     t_wall = time.perf_counter()
-    e0.record(stream)
-    for _ in range(args.steps):
-        step()
-    e1.record(stream)
-    torch.cuda.synchronize()
-    t_wall = time.perf_counter() - t_wall
-    ms_step = e0.elapsed_time(e1) / args.steps
-    print(f"# timed {args.steps} steps: {ms_step:.3f} ms/step (wall {t_wall / args.steps * 1e3:.3f})",
-          file=sys.stderr, flush=True)
-
-    # ---- per-op durations: mean launch duration, HIP events on the launch stream ----
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(ops) + 1)] for _ in range(args.steps)]
+    marks[0].record(stream)
     for it in range(args.steps):
-        evs[it][0].record(stream)
         for i, (_, f) in enumerate(ops):
             f()
-            evs[it][i + 1].record(stream)
+            marks[1 + it * nops + i].record(stream)
     torch.cuda.synchronize()
-    op_ms = {name: float(np.mean([evs[it][i].elapsed_time(evs[it][i + 1]) for it in range(args.steps)]))
+    t_wall = time.perf_counter() - t_wall
+    ms_step = marks[0].elapsed_time(marks[-1]) / args.steps
+    print(f"# timed {args.steps} steps: {ms_step:.3f} ms/step (wall {t_wall / args.steps * 1e3:.3f})",
+          file=sys.stderr, flush=True)
+    op_ms = {name: float(np.mean([marks[it * nops + i].elapsed_time(marks[it * nops + i + 1])
+                                  for it in range(args.steps)]))
              for i, (name, _) in enumerate(ops)}
+
     cold = cold_steps(step, stream, args.steps)
     cold["tokens_per_s"] = round(Nb * L / (cold["ms_per_step"] * 1e-3), 1)
 
