@@ -85,6 +85,8 @@ def cpu_baseline(d, cfg, rows):
     dt = time.perf_counter() - t0
     tokens = rows * cfg.seqlen
     return {"value": tokens / dt, "unit": "tokens/s", "cores": O.num_threads(), "kind": "oracle",
+            "cores_note": f"OpenMP threads the oracle ran with; {len(os.sched_getaffinity(0))} CPUs in the "
+                          "process's affinity mask",
             "sample": f"batch rows 0..{rows - 1} of the same workload ({tokens} tokens x {cfg.dim} "
                       f"channels), conv1d + selective scan forward and backward in fp64",
             "seconds": dt}
@@ -424,6 +426,8 @@ def main():
     ap.add_argument("--no-compare", action="store_true",
                     help="skip the padded / single-sequence runs of the same tokens (Mamba-1.4B shape only)")
     ap.add_argument("--cpu-rows", type=int, default=8)
+    ap.add_argument("--no-workloads", action="store_true",
+                    help="at the Mamba-1.4B shape, skip the other workloads (configs 1, 3, 4a, 4b, fp32, random A)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only copy BYTES with a plain device copy (calibrates HBM byte counters)")
     args = ap.parse_args()
@@ -460,95 +464,56 @@ def main():
         __graft_entry__.build()
     lib = _lib.load()
     dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
     cfg = W.config(args.config, **({"dtype": args.dtype} if args.dtype else {}))
     Nb, Dn, L, N, Wd = cfg.batch, cfg.dim, cfg.seqlen, cfg.dstate, cfg.width
     code = _lib.BF16 if cfg.dtype == "bf16" else _lib.F32
-    tdt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
-    s = 2 if cfg.dtype == "bf16" else 4
 
-    print(f"# generating config {cfg.key} inputs {Nb}x{Dn}x{L}", file=sys.stderr, flush=True)
-    d = W.make_inputs(cfg, variant=args.variant)
-
-    def act(a):
-        return torch.from_numpy(a).to(tdt).to(dev)
-
-    def f32(a):
-        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
-
-    tens = {k: act(d[k]) for k in ("x", "delta", "z", "B", "C", "dout")}
-    tens.update({k: f32(d[k]) for k in ("A", "D", "delta_bias", "w", "bias")})
-    tens["pos"] = torch.from_numpy(d["pos"]).to(dev)
-    stream = torch.cuda.current_stream(dev)
-    chain = Chain(lib, tens, code, Wd, stream)
-    ops = chain.ops()
-
-    def step():
-        for _, f in ops:
-            f()
-
-    print("# warmup", file=sys.stderr, flush=True)
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-
-    # ---- timed region: exactly K steps, with a HIP event on the launch stream after every
-    # op, so that each op's mean launch duration comes from the timed steps themselves ----
-    nops = len(ops)
-    marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps * nops + 1)]
-    torch.cuda.synchronize()
-    t_wall = time.perf_counter()
-    marks[0].record(stream)
-    for it in range(args.steps):
-        for i, (_, f) in enumerate(ops):
-            f()
-            marks[1 + it * nops + i].record(stream)
-    torch.cuda.synchronize()
-    t_wall = time.perf_counter() - t_wall
-    ms_step = marks[0].elapsed_time(marks[-1]) / args.steps
-    print(f"# timed {args.steps} steps: {ms_step:.3f} ms/step (wall {t_wall / args.steps * 1e3:.3f})",
+    head = run_workload(lib, cfg, args.variant, args.steps, args.warmup, stream, keep=True)
+    print(f"# timed {args.steps} steps: median {head['ms_per_step']:.3f} ms/step, mean {head['mean_ms_per_step']:.3f}",
           file=sys.stderr, flush=True)
-    op_ms = {name: float(np.mean([marks[it * nops + i].elapsed_time(marks[it * nops + i + 1])
-                                  for it in range(args.steps)]))
-             for i, (name, _) in enumerate(ops)}
+    d, tens, step = head.pop("_d"), head.pop("_tens"), head.pop("_step")
+    op_ms = {k: v["ms"] for k, v in head["ops"].items()}
 
     cold = cold_steps(step, stream, args.steps)
     cold["tokens_per_s"] = round(Nb * L / (cold["ms_per_step"] * 1e-3), 1)
 
-    mb = minimal_bytes(Nb, Dn, L, N, Wd, s)
-    total_bytes = sum(mb.values())
-    tokens = Nb * L
-    value = tokens / (ms_step * 1e-3)
+    mb = minimal_bytes(Nb, Dn, L, N, Wd, 2 if cfg.dtype == "bf16" else 4)
     E = Nb * Dn * L
     bwd_s = op_ms["scan_bwd"] * 1e-3
     achieved = E * N * SLOTS_BWD / bwd_s / 1e12
     peak = VALU_PEAK / 1e12
     traffic = stored_traffic({"batch": Nb, "seqlen": L, "dim": Dn, "dstate": N, "storage": cfg.dtype})
     roof = {
+        # the dominant kernel is issue-bound (plain fp32 VALU arithmetic): its roofline is the
+        # VALU issue rate; the metric's own roofline, HBM, is reported beside it
         "bound": "alu", "achieved": round(achieved, 3), "peak": round(peak, 3), "unit": "Tslot/s",
         "frac": round(achieved / peak, 4),
         "traffic": (traffic["bytes_per_launch"] if traffic else None),
-        "kernel": "selective_scan_bwd (main kernel + two finalize kernels, one ABI call)",
+        "traffic_source": ("replayed from the stored rocprofv3 FETCH_SIZE/WRITE_SIZE run "
+                           "profiles/scan_bwd_traffic_mamba1.4b_step.json (same kernel source hash and shape), "
+                           "not measured in this run" if traffic else None),
+        "kernel": "selective_scan_bwd (main kernel + finalize kernels, one ABI call)",
         "duration_ms": round(op_ms["scan_bwd"], 4),
-        "hbm_frac_of_minimal_bytes": round(mb["scan_bwd"] / bwd_s / HBM_PEAK, 4),
+        "hbm": {"bound": "hbm", "achieved": round(mb["scan_bwd"] / bwd_s / 1e9, 1), "peak": HBM_PEAK / 1e9,
+                "unit": "GB/s", "frac": round(mb["scan_bwd"] / bwd_s / HBM_PEAK, 4),
+                "bytes_per_launch": int(mb["scan_bwd"])},
+        "metric_roofline": "hbm (the metric's % of HBM peak: roofline.hbm.frac for this kernel, "
+                           "hbm_frac / scan_hbm_frac for the step)",
     }
     line = {
-        "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
-        "data": "synthetic",
-        "config": {
-            "workload": f"{cfg.name} layer: {Nb} packed rows x {L} tokens, d_inner {Dn}, d_state {N}, "
-                        f"conv width {Wd}, {cfg.dtype} activations, fp32 state; sequence lengths "
-                        f"{cfg.lengths[0]}{tuple(cfg.lengths[1:])} packed sequentially",
-            "batch": Nb, "seqlen": L, "dim": Dn, "dstate": N, "width": Wd, "storage": cfg.dtype,
-            "sequences": int(len(d["lengths"])), "variant": args.variant,
-        },
-        "hbm_frac": round(total_bytes / (ms_step * 1e-3) / HBM_PEAK, 4),
-        "minimal_bytes_per_step": int(total_bytes),
-        "ops": {k: {"ms": round(v, 4), "minimal_GBps": round(mb[k] / (v * 1e-3) / 1e9, 1),
-                    "hbm_frac": round(mb[k] / (v * 1e-3) / HBM_PEAK, 4)} for k, v in op_ms.items()},
-        "scan_hbm_frac": round((mb["scan_fwd"] + mb["scan_bwd"]) /
-                               ((op_ms["scan_fwd"] + op_ms["scan_bwd"]) * 1e-3) / HBM_PEAK, 4),
+        "metric": METRIC, "value": round(Nb * L / (head["ms_per_step"] * 1e-3), 1), "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": head["ms_per_step"],
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": cfg.dtype, "data": "synthetic",
+        "config": head["config"],
+        "mean_ms_per_step": head["mean_ms_per_step"],
+        "timing": "ms_per_step and per-op ms are medians over the K timed steps (HIP events on the launch "
+                  "stream after every ABI call); value = tokens / median step",
+        "hbm_frac": head["hbm_frac"],
+        "minimal_bytes_per_step": head["minimal_bytes_per_step"],
+        "ops": head["ops"],
+        "scan_hbm_frac": head["scan_hbm_frac"],
         "roofline": roof,
         "cold_cache": cold,
         "device": torch.cuda.get_device_name(0),
@@ -559,13 +524,102 @@ def main():
                                             packed_step=step)
         print("# comparison: padded and single-sequence runs of the same tokens", file=sys.stderr, flush=True)
         line["comparison"] = comparison(lib, tens, d["pos"], code, Wd, stream, steps=5, warmup=2,
-                                        packed_ms=ms_step)
+                                        packed_ms=head["ms_per_step"])
     if cfg.lengths[0] == "lognormal":
         line["packing_padding"] = packing_rates(cfg.lengths, L)
+    cpu_d = d
+    del tens, step
+    torch.cuda.empty_cache()
+    if args.config == "2" and not args.no_workloads:
+        # every other workload, through the same step: the other layer shapes, the boundary
+        # stress and long-row rows, fp32 activations, and random parameter values
+        extra = {}
+        for key, name, kw, var in (("1", "1", {}, "paper"), ("3", "3", {}, "paper"), ("4a", "4a", {}, "paper"),
+                                   ("4b", "4b", {}, "paper"), ("2", "2-f32", {"dtype": "f32"}, "paper"),
+                                   ("2", "2-general", {}, "general")):
+            print(f"# workload {name}", file=sys.stderr, flush=True)
+            r = run_workload(lib, W.config(key, **kw), var, args.steps, args.warmup, stream)
+            r.pop("minimal_bytes_per_step")
+            extra[name] = r
+            torch.cuda.empty_cache()
+        line["workloads"] = extra
     if not args.no_cpu_baseline:
         print("# cpu baseline (oracle)", file=sys.stderr, flush=True)
-        line["cpu_baseline"] = cpu_baseline(d, cfg, args.cpu_rows)
+        line["cpu_baseline"] = cpu_baseline(cpu_d, cfg, args.cpu_rows)
     print(json.dumps(line), flush=True)
+
+
+def run_workload(lib, cfg, variant, steps, warmup, stream, keep=False):
+    """Synthetic inputs of one workload on the device, K timed steps after W warm-ups, with
+    a HIP event after every ABI call of every timed step: median step and per-op times,
+    the minimal bytes of each op and the resulting fractions of the HBM peak."""
+    import numpy as np
+    import torch
+    import workloads as W
+    from paper_2408_03865_amd import _lib
+    dev = stream.device
+    Nb, Dn, L, N, Wd = cfg.batch, cfg.dim, cfg.seqlen, cfg.dstate, cfg.width
+    code = _lib.BF16 if cfg.dtype == "bf16" else _lib.F32
+    tdt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    s = 2 if cfg.dtype == "bf16" else 4
+    print(f"# generating config {cfg.key} inputs {Nb}x{Dn}x{L} {cfg.dtype} {variant}", file=sys.stderr, flush=True)
+    d = W.make_inputs(cfg, variant=variant)
+    tens = {k: torch.from_numpy(d[k]).to(tdt).to(dev) for k in ("x", "delta", "z", "B", "C", "dout")}
+    tens.update({k: torch.from_numpy(np.ascontiguousarray(d[k], dtype=np.float32)).to(dev)
+                 for k in ("A", "D", "delta_bias", "w", "bias")})
+    tens["pos"] = torch.from_numpy(d["pos"]).to(dev)
+    chain = Chain(lib, tens, code, Wd, stream)
+    ops = chain.ops()
+
+    def step():
+        for _, f in ops:
+            f()
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    # timed region: exactly K steps, with a HIP event on the launch stream after every op
+    nops = len(ops)
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(steps * nops + 1)]
+    torch.cuda.synchronize()
+    marks[0].record(stream)
+    for it in range(steps):
+        for i, (_, f) in enumerate(ops):
+            f()
+            marks[1 + it * nops + i].record(stream)
+    torch.cuda.synchronize()
+    total = marks[0].elapsed_time(marks[-1])
+    per_step = [marks[it * nops].elapsed_time(marks[(it + 1) * nops]) for it in range(steps)]
+    op_ms = {name: float(np.median([marks[it * nops + i].elapsed_time(marks[it * nops + i + 1])
+                                    for it in range(steps)]))
+             for i, (name, _) in enumerate(ops)}
+    ms = float(np.median(per_step))
+    mb = minimal_bytes(Nb, Dn, L, N, Wd, s)
+    total_bytes = sum(mb.values())
+    res = {
+        "config": {
+            "workload": f"{cfg.name} layer: {Nb} packed rows x {L} tokens, d_inner {Dn}, d_state {N}, "
+                        f"conv width {Wd}, {cfg.dtype} activations, fp32 state; sequence lengths "
+                        f"{cfg.lengths[0]}{tuple(cfg.lengths[1:])}",
+            "batch": Nb, "seqlen": L, "dim": Dn, "dstate": N, "width": Wd, "storage": cfg.dtype,
+            "arithmetic": "f32", "sequences": int(len(d["lengths"])), "variant": variant,
+        },
+        "ms_per_step": round(ms, 4),
+        "mean_ms_per_step": round(total / steps, 4),
+        "tokens_per_s": round(Nb * L / (ms * 1e-3), 1),
+        "hbm_frac": round(total_bytes / (ms * 1e-3) / HBM_PEAK, 4),
+        "minimal_bytes_per_step": int(total_bytes),
+        "ops": {k: {"ms": round(v, 4), "minimal_GBps": round(mb[k] / (v * 1e-3) / 1e9, 1),
+                    "hbm_frac": round(mb[k] / (v * 1e-3) / HBM_PEAK, 4)} for k, v in op_ms.items()},
+        "scan_hbm_frac": round((mb["scan_fwd"] + mb["scan_bwd"]) /
+                               ((op_ms["scan_fwd"] + op_ms["scan_bwd"]) * 1e-3) / HBM_PEAK, 4),
+        "scan_bwd_alu_frac": round(Nb * Dn * L * N * SLOTS_BWD / (op_ms["scan_bwd"] * 1e-3) / VALU_PEAK, 4),
+    }
+    if keep:
+        res.update(_d=d, _tens=tens, _step=step)
+    else:
+        del chain, ops, tens
+    return res
 
 
 if __name__ == "__main__":

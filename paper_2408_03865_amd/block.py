@@ -102,8 +102,13 @@ def block_forward(x, pos, p: Dict[str, object], mark: Optional[Callable[[str], N
     return out, ctx
 
 
-def block_backward(dout, ctx, p, mark: Optional[Callable[[str], None]] = None) -> Dict[str, object]:
-    """Gradients of sum(dout * out) with respect to x and every parameter."""
+def block_backward(dout, ctx, p, mark: Optional[Callable[[str], None]] = None,
+                   trace: Optional[Dict[str, object]] = None) -> Dict[str, object]:
+    """Gradients of sum(dout * out) with respect to x and every parameter.  With ``trace``
+    (a dict), the backward's own intermediates are left in it: the scan's upstream
+    gradient dy and its outputs scan (scan_du: its du before the x projection's
+    gradient is added in place), the conv's upstream gradient du and its dx dxi,
+    and the RMSNorm's upstream gradient dh."""
     mk = mark or (lambda name: None)
     Dn = p["D"].shape[0]
     Wx = p["W_x"]
@@ -121,6 +126,8 @@ def block_backward(dout, ctx, p, mark: Optional[Callable[[str], None]] = None) -
     ddtl = _lin_dx(p["W_dt"], s["ddelta"])
     dxdbl = _torch().cat([ddtl, s["dB"].to(dt), s["dC"].to(dt)], 1)      # (batch, R + 2N, L)
     g["W_x"] = _lin_dw_thin(dxdbl, ctx["u"])
+    if trace is not None:
+        trace["scan_du"] = s["du"].clone()       # the scan's own du, before the sum below
     du = s["du"].baddbmm_(_bcast(Wx.t(), dxdbl.shape[0]), dxdbl)   # accumulated into the scan's du
     mk("conv_bwd")
     dxi, g["conv_w"], g["conv_b"] = P.causal_conv1d_bwd(ctx["xi"], p["conv_w"], p["conv_b"], ctx["pos"],
@@ -133,4 +140,6 @@ def block_backward(dout, ctx, p, mark: Optional[Callable[[str], None]] = None) -
     # the residual's gradient (dout itself) is added inside the RMSNorm backward
     g["x"], g["norm_w"] = P.rmsnorm_bwd(ctx["x"], p["norm_w"], ctx["r"], dh, dresidual=dout)
     mk("end")
+    if trace is not None:
+        trace.update(dy=dy, scan=s, du=du, dxi=dxi, dh=dh)
     return g

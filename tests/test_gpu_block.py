@@ -1,7 +1,8 @@
 """GPU parity of the packed Mamba block (paper_2408_03865_amd/block.py): forward and every
-gradient against the fp64 block oracle (fp32 path; the bf16 path re-rounds every GEMM
-output, so its block chain is not compared with an unrounded oracle chain -- the
-per-operator bf16 parity covers the kernels), and packing-unpacking invariance on the GPU."""
+gradient against the fp64 block oracle (fp32 path); the bf16 block operator by operator on
+its own device intermediates (the bf16 path re-rounds every GEMM output, so its block
+chain is not compared with an unrounded oracle chain); and packing-unpacking invariance
+on the GPU."""
 import numpy as np
 import pytest
 
@@ -85,3 +86,90 @@ def test_block_pui_on_gpu():
     torch.cuda.synchronize()
     for k in acc:
         assert_close(f"pui d{k}", host(g[k]), acc[k], TOL["f32"])
+
+
+def test_block_bf16_per_op():
+    """The bf16 block (bf16 activations and projection weights, what the block benchmark
+    runs), checked operator by operator on the block's own device intermediates: each
+    library op is run again on exactly the bf16 tensors the block fed it, with fp32
+    outputs (dtype code 2), and compared with the fp64 oracle of that op against the bf16
+    bound; the block's own bf16 outputs of the op must be the round-to-nearest-even of
+    those fp32 outputs bit for bit, and its fp32-typed outputs identical.  (The GEMMs
+    between the ops round their outputs to bf16, so the whole bf16 chain is not compared
+    with an unrounded oracle chain.)"""
+    import torch
+    import oracle as O
+    import oracle.block as OB
+    import paper_2408_03865_amd as P
+    import paper_2408_03865_amd.block as BK
+    from gpu_common import bf16_bits_of, rne_bf16
+
+    batch, L = 2, 777
+    bf = torch.bfloat16
+    p = _params(**DIMS, seed=31)
+    rng = np.random.default_rng(32)
+    rows = W.draw_row_lengths(("lognormal", 4.0, 1.0, 1, L), rng, batch, L)
+    pos = i32(W.positions_from_lengths(rows, L))
+    pos64 = host(pos).astype(np.int32)
+    gp = _to_gpu(p)
+    for k in ("W_in", "W_x", "W_dt", "W_out"):
+        gp[k] = gp[k].to(bf)
+    x = f32(rng.standard_normal((batch, DIMS["d_model"], L)).astype(np.float32)).to(bf)
+    dout = f32(rng.standard_normal((batch, DIMS["d_model"], L)).astype(np.float32)).to(bf)
+    out, ctx = BK.block_forward(x, pos, gp)
+    tr = {}
+    g = BK.block_backward(dout, ctx, gp, trace=tr)
+    torch.cuda.synchronize()
+    tol = TOL["bf16"]
+    w = {k: host(v) for k, v in gp.items() if v.dtype == torch.float32}
+
+    def same_bits(name, got_bf, ref_f32):
+        bad = np.count_nonzero(bf16_bits_of(got_bf) != rne_bf16(ref_f32))
+        assert bad == 0, f"{name}: {bad} bf16 outputs differ from RNE of the fp32 outputs"
+
+    # RMSNorm forward
+    h32, r32 = P.rmsnorm_fwd(x, gp["norm_w"], BK.EPS, out_f32=True)
+    same_bits("rmsnorm out", ctx["h"], h32)
+    assert torch.equal(ctx["r"], r32)
+    href, rref = OB.rmsnorm(host(x), w["norm_w"], BK.EPS)
+    assert_close("rmsnorm out", host(h32), href, tol)
+    assert_close("rmsnorm rstd", host(r32), rref[:, 0, :], tol)
+    # conv forward (+ SiLU)
+    u32 = P.causal_conv1d_fwd(ctx["xi"], gp["conv_w"], gp["conv_b"], pos, silu=True, out_f32=True)
+    same_bits("conv out", ctx["u"], u32)
+    assert_close("conv out", host(u32), O.conv1d_fwd(host(ctx["xi"]), w["conv_w"], w["conv_b"], pos64), tol)
+    # scan forward
+    sargs = dict(A=gp["A"], B=ctx["B"], C=ctx["C"], D=gp["D"], z=ctx["z"], delta_bias=gp["dt_bias"],
+                 delta_softplus=True, position_indices=pos)
+    y32 = P.selective_scan_fwd(ctx["u"], ctx["delta"], **sargs, out_f32=True)
+    same_bits("scan out", ctx["y"], y32)
+    oargs = dict(u=host(ctx["u"]), delta=host(ctx["delta"]), A=w["A"], B=host(ctx["B"]), C=host(ctx["C"]),
+                 D=w["D"], z=host(ctx["z"]), delta_bias=w["dt_bias"], delta_softplus=True, pos=pos64)
+    assert_close("scan out", host(y32), O.scan_fwd(**oargs), tol)
+    # scan backward, on the block's upstream gradient dy
+    s32 = P.selective_scan_bwd(ctx["u"], ctx["delta"], **sargs, dout=tr["dy"], saved_states=ctx["st"],
+                               out_f32=True)
+    sb = dict(tr["scan"], du=tr["scan_du"])
+    for k in ("du", "ddelta", "dz"):
+        same_bits(f"scan {k}", sb[k], s32[k])
+    for k in ("dA", "dB", "dC", "dD", "ddelta_bias"):
+        assert torch.equal(sb[k], s32[k]), k
+    sref = O.scan_bwd(**oargs, dout=host(tr["dy"]))
+    for k in ("du", "ddelta", "dz", "dA", "dB", "dC", "dD", "ddelta_bias"):
+        assert_close(f"scan {k}", host(s32[k]), sref[k], tol)
+    # conv backward, on the block's upstream gradient du (the scan's du plus the x projection's)
+    dx32, dw32, db32 = P.causal_conv1d_bwd(ctx["xi"], gp["conv_w"], gp["conv_b"], pos, tr["du"], silu=True,
+                                           out_f32=True)
+    same_bits("conv dx", tr["dxi"], dx32)
+    assert torch.equal(g["conv_w"], dw32) and torch.equal(g["conv_b"], db32)
+    cref = O.conv1d_bwd(host(ctx["xi"]), w["conv_w"], w["conv_b"], pos64, host(tr["du"]))
+    for k, v in (("dx", dx32), ("dw", dw32), ("dbias", db32)):
+        assert_close(f"conv {k}", host(v), cref[k], tol)
+    # RMSNorm backward, with the residual's gradient added
+    gx32, gw32 = P.rmsnorm_bwd(x, gp["norm_w"], ctx["r"], tr["dh"], dresidual=dout, out_f32=True)
+    same_bits("rmsnorm dx", g["x"], gx32)
+    assert torch.equal(g["norm_w"], gw32)
+    dxn, dwn = OB.rmsnorm_bwd(host(x), w["norm_w"], host(ctx["r"])[:, None, :], host(tr["dh"]))
+    assert_close("rmsnorm dx", host(gx32), dxn + host(dout), tol)
+    assert_close("rmsnorm dweight", host(gw32), dwn, tol)
+    note("bf16 block: every op matches the oracle on the block's own intermediates")

@@ -4,7 +4,8 @@ import numpy as np
 import pytest
 
 import workloads as W
-from gpu_common import PER_B, PER_CHANNEL, PER_TOKEN, TOL, compare, gpu_inputs, host, i32, note, oracle_run, run_gpu
+from gpu_common import (PER_B, PER_CHANNEL, PER_TOKEN, TOL, check_bf16_rounding, compare, gpu_inputs, host, i32,
+                        note, oracle_run, run_gpu)
 
 pytestmark = pytest.mark.gpu
 
@@ -28,6 +29,10 @@ def test_ragged_shapes(shape, dtype):
     g = gpu_inputs(d, dtype)
     r = run_gpu(g, out_f32=(dtype == "bf16"))
     compare(r, oracle_run(d), TOL[dtype], ALL, label=f"{shape} {dtype} ")
+    if dtype == "bf16":
+        # the bf16-output kernels (what the benchmark runs), including their scalar tail
+        # stores at lengths that are not multiples of the 8-token vectors
+        check_bf16_rounding(run_gpu(g, out_f32=False), r, f"{shape} bf16-out ")
 
 
 # Shapes with at least 768 blocks of 16 channels: the scans keep one segment per row
@@ -174,19 +179,28 @@ EXTREME = [(48, 256, 520), (1, 16, 6000)]
 
 
 def _compare_normwise(gr, ref, tol, label):
-    worst = {}
+    """Asserts the widened bound; reports, per tensor, the worst error over the stated
+    element-wise bound tol (1 + |ref|) alone as well (a ratio above 1 there says where the
+    floor is what keeps the tensor in bounds)."""
+    worst, stated = {}, {}
     for k in ALL:
         if ref.get(k) is None:
             continue
         got = np.asarray(host(gr[k]), dtype=np.float64)
         r = np.asarray(ref[k], dtype=np.float64)
         assert got.shape == r.shape and np.all(np.isfinite(got)), k
-        bound = tol * (1.0 + np.abs(r)) + 16.0 * 2.0 ** -24 * float(np.abs(r).max())
-        ratio = np.abs(got - r) / bound
+        elem = tol * (1.0 + np.abs(r))
+        bound = elem + 16.0 * 2.0 ** -24 * float(np.abs(r).max())
+        err = np.abs(got - r)
+        ratio = err / bound
         i = np.unravel_index(int(np.argmax(ratio)), ratio.shape)
         assert ratio[i] <= 1.0, f"{label}{k}: error {abs(got[i] - r[i]):.3e} over bound {bound[i]:.3e} at {i}: got {got[i]!r} ref {r[i]!r}"
         worst[k] = float(ratio[i])
+        stated[k] = float(np.max(err / elem))
     note(f"{label} worst error / bound: " + ", ".join(f"{k}={v:.2e}" for k, v in worst.items()))
+    note(f"{label} worst error / stated element-wise bound: " +
+         ", ".join(f"{k}={v:.2e}{'' if v <= 1.0 else ' (over)'}" for k, v in stated.items()))
+    return stated
 
 
 @pytest.mark.parametrize("shape", EXTREME, ids=lambda s: "x".join(map(str, s)))

@@ -77,7 +77,7 @@ def test_scan_probe(key, out_f32):
     assert np.all(np.abs(dA[:, 0] - want_dA0) <= 1e-4 * (1 + abs(want_dA0))), (dA[:4, 0], want_dA0)
 
 
-@pytest.mark.parametrize("key,out_f32", [("0", True), ("1", True), ("2", True), ("4a", True),
+@pytest.mark.parametrize("key,out_f32", [("0", True), ("1", True), ("2", True), ("3", True), ("4a", True),
                                          ("4a", False), ("4b", True)])
 @pytest.mark.parametrize("width", [4, 3, 2])
 def test_conv_probe(key, out_f32, width):

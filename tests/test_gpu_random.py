@@ -8,7 +8,8 @@ import numpy as np
 import pytest
 
 import workloads as W
-from gpu_common import PER_B, PER_CHANNEL, PER_TOKEN, TOL, compare, gpu_inputs, note, oracle_run, run_gpu
+from gpu_common import (PER_B, PER_CHANNEL, PER_TOKEN, TOL, check_bf16_rounding, compare, gpu_inputs, note,
+                        oracle_run, run_gpu)
 
 pytestmark = pytest.mark.gpu
 
@@ -34,5 +35,8 @@ def test_random_case(i):
     note(f"random case {i}: batch {batch} dim {dim} seqlen {seqlen} width {width} {dtype} {law} {variant}")
     cfg = W.Config("random", "random", batch, seqlen, dim, 16, width, dtype, law, 9200 + i)
     d = W.make_inputs(cfg, variant=variant)
-    r = run_gpu(gpu_inputs(d, dtype), out_f32=(dtype == "bf16"))
+    g = gpu_inputs(d, dtype)
+    r = run_gpu(g, out_f32=(dtype == "bf16"))
     compare(r, oracle_run(d), TOL[dtype], ALL, label=f"random {i} ")
+    if dtype == "bf16":
+        check_bf16_rounding(run_gpu(g, out_f32=False), r, f"random {i} bf16-out ")
