@@ -13,7 +13,9 @@
  *  - Every pointer is a DEVICE pointer owned by the caller.  The library never
  *    allocates, frees or synchronises; it only enqueues kernels on `stream`
  *    (a hipStream_t; NULL means the null stream).  It keeps no mutable global
- *    state, so concurrent calls on different streams are independent.
+ *    state, so concurrent calls on different streams are independent -- except
+ *    packmamba_causal_conv1d_bwd_noalloc, whose fixed scratch buffer is shared by
+ *    every call on a device (see there).
  *  - Layout: contiguous, row-major, sequence axis innermost:
  *      activations (x, u, delta, z, out, dout and their gradients)  (batch, dim, seqlen)
  *      B, C, dB, dC                                                 (batch, dstate, seqlen)
@@ -54,7 +56,7 @@
 extern "C" {
 #endif
 
-#define PACKMAMBA_ABI_VERSION 5
+#define PACKMAMBA_ABI_VERSION 6
 
 /* dtype codes of the activation tensors */
 #define PACKMAMBA_F32 0            /* fp32 inputs, fp32 outputs */
@@ -72,7 +74,8 @@ typedef enum {
     PACKMAMBA_ERR_UNSUPPORTED = 3,  /* dtype, width (2..4) or dstate (16) not supported */
     PACKMAMBA_ERR_ALIGN = 4,        /* a pointer is not 16-byte aligned */
     PACKMAMBA_ERR_WORKSPACE = 5,    /* workspace NULL or smaller than the *_workspace_size() result */
-    PACKMAMBA_ERR_LAUNCH = 6        /* the HIP runtime rejected a kernel launch */
+    PACKMAMBA_ERR_LAUNCH = 6,       /* the HIP runtime rejected a kernel launch */
+    PACKMAMBA_ERR_SCRATCH = 7       /* the shape needs more than the fixed scratch of a no-allocation entry point */
 } packmamba_status;
 
 /* ABI version of the loaded library (PACKMAMBA_ABI_VERSION). */
@@ -125,6 +128,35 @@ int packmamba_causal_conv1d_bwd(const void* x, const float* weight, const float*
                                 void* workspace, size_t workspace_bytes,
                                 int64_t batch, int64_t dim, int64_t seqlen, int32_t width,
                                 int32_t dtype, int32_t silu, void* stream);
+
+/* Size of the fixed scratch of packmamba_causal_conv1d_bwd_noalloc, in bytes. */
+#define PACKMAMBA_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
+
+/*
+ * packmamba_causal_conv1d_bwd without a workspace argument, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops, and
+ * harnesses that forbid hipMalloc.  Same arguments (minus the workspace), results
+ * and errors as packmamba_causal_conv1d_bwd, whose kernels it runs; the per-row
+ * parameter-gradient partials live in a file-scope device array of
+ * PACKMAMBA_NOALLOC_SCRATCH_BYTES that each GPU the library runs on holds until the
+ * process ends.  The call itself allocates nothing (no hipMalloc, hipFree or
+ * allocating library routine); the array's device address is looked up once per
+ * device, on that device's first call.
+ *   A shape whose packmamba_causal_conv1d_bwd_workspace_size() exceeds
+ *   PACKMAMBA_NOALLOC_SCRATCH_BYTES returns PACKMAMBA_ERR_SCRATCH before anything
+ *   is enqueued (e.g. batch * dim * (width + 1) * 4 bytes above 16 MiB for rows
+ *   that are not split).
+ *   Every call on a GPU shares that GPU's scratch and leaves its contents behind:
+ *   calls that overlap on one GPU (concurrent streams, or threads) race and must
+ *   be serialised by the caller.  Every scratch element a call reads is written
+ *   by the same call first, so nothing needs clearing between calls.
+ */
+int packmamba_causal_conv1d_bwd_noalloc(const void* x, const float* weight, const float* bias,
+                                        const int32_t* position_indices, const void* initial_x,
+                                        const void* dout, const void* dfinal_x,
+                                        void* dx, float* dweight, float* dbias, void* dinitial_x,
+                                        int64_t batch, int64_t dim, int64_t seqlen, int32_t width,
+                                        int32_t dtype, int32_t silu, void* stream);
 
 /* Bytes of the optional saved-states buffer of packmamba_selective_scan_fwd: the
  * chunk states, (batch, dim, ceil(seqlen / PACKMAMBA_STATE_STRIDE), dstate) floats,

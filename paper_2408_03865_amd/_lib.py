@@ -16,10 +16,11 @@ LIB_PATH = os.path.join(HERE, "libpackmamba.so")
 
 F32, BF16, BF16_F32OUT = 0, 1, 2
 STATE_STRIDE = 128
-ABI_VERSION = 5
+ABI_VERSION = 6
 
 STATUS = {0: "OK", 1: "ERR_NULL", 2: "ERR_SHAPE", 3: "ERR_UNSUPPORTED", 4: "ERR_ALIGN",
-          5: "ERR_WORKSPACE", 6: "ERR_LAUNCH"}
+          5: "ERR_WORKSPACE", 6: "ERR_LAUNCH", 7: "ERR_SCRATCH"}
+NOALLOC_SCRATCH_BYTES = 16 << 20
 
 # Every symbol the header declares.
 EXPORTS = (
@@ -30,6 +31,7 @@ EXPORTS = (
     "packmamba_selective_scan_bwd_workspace_size", "packmamba_selective_scan_bwd",
     "packmamba_check_position_indices", "packmamba_pack_plan", "packmamba_pack_positions",
     "packmamba_rmsnorm_fwd", "packmamba_rmsnorm_bwd_workspace_size", "packmamba_rmsnorm_bwd",
+    "packmamba_causal_conv1d_bwd_noalloc",
 )
 
 PACK_SEQUENTIAL, PACK_GREEDY, PACK_CUT = 0, 1, 2
@@ -78,6 +80,7 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.packmamba_causal_conv1d_bwd_workspace_size.argtypes = [i64, i64, i64, i32]
     lib.packmamba_causal_conv1d_bwd_workspace_size.restype = sz
     lib.packmamba_causal_conv1d_bwd.argtypes = [vp] * 12 + [sz, i64, i64, i64, i32, i32, i32, vp]
+    lib.packmamba_causal_conv1d_bwd_noalloc.argtypes = [vp] * 11 + [i64, i64, i64, i32, i32, i32, vp]
     lib.packmamba_selective_scan_fwd_saved_states_size.argtypes = [i64, i64, i64, i32]
     lib.packmamba_selective_scan_fwd_saved_states_size.restype = sz
     lib.packmamba_selective_scan_fwd_workspace_size.argtypes = [i64, i64, i64, i32]
@@ -94,7 +97,7 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.packmamba_rmsnorm_bwd_workspace_size.restype = sz
     lib.packmamba_rmsnorm_bwd.argtypes = [vp] * 8 + [sz, i64, i64, i64, i32, vp]
     for name in ("packmamba_pack_plan", "packmamba_pack_positions", "packmamba_causal_conv1d_fwd",
-                 "packmamba_causal_conv1d_bwd",
+                 "packmamba_causal_conv1d_bwd", "packmamba_causal_conv1d_bwd_noalloc",
                  "packmamba_selective_scan_fwd", "packmamba_selective_scan_bwd",
                  "packmamba_check_position_indices", "packmamba_rmsnorm_fwd", "packmamba_rmsnorm_bwd"):
         getattr(lib, name).restype = ctypes.c_int

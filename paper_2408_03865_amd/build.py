@@ -15,7 +15,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 OUT_DIR = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libpackmamba.so")
-SOURCES = ["api.cpp", "pack.cpp", "conv1d.hip", "scan_fwd.hip", "scan_bwd.hip", "check_pos.hip", "rmsnorm.hip"]
+SOURCES = ["api.cpp", "pack.cpp", "conv1d.hip", "scan_fwd.hip", "scan_bwd.hip", "check_pos.hip", "rmsnorm.hip",
+           "noalloc.hip"]
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -97,6 +97,27 @@ int launch_status(hipError_t e) { return e == hipSuccess ? PACKMAMBA_OK : PACKMA
 
 }  // namespace
 
+namespace pm {
+
+int conv1d_bwd_args_status(const void* x, const float* weight, const float* bias, const int32_t* position_indices,
+                           const void* initial_x, const void* dout, const void* dfinal_x, const void* dx,
+                           const float* dweight, const float* dbias, const void* dinitial_x, int64_t batch,
+                           int64_t dim, int64_t seqlen, int32_t width, int32_t dtype) {
+    if (!x || !weight || !position_indices || !dout || !dx || !dweight) return PACKMAMBA_ERR_NULL;
+    if ((bias == nullptr) != (dbias == nullptr)) return PACKMAMBA_ERR_NULL;
+    if ((initial_x == nullptr) != (dinitial_x == nullptr)) return PACKMAMBA_ERR_NULL;
+    if (int e = check_shape(batch, dim, seqlen)) return e;
+    if (int e = check_dtype(dtype)) return e;
+    if (width < 2 || width > 4) return PACKMAMBA_ERR_UNSUPPORTED;
+    if (!aligned16(x) || !aligned16(weight) || !aligned16(bias) || !aligned16(position_indices) ||
+        !aligned16(dout) || !aligned16(dx) || !aligned16(dweight) || !aligned16(dbias) ||
+        !aligned16(initial_x) || !aligned16(dfinal_x) || !aligned16(dinitial_x))
+        return PACKMAMBA_ERR_ALIGN;
+    return PACKMAMBA_OK;
+}
+
+}  // namespace pm
+
 extern "C" {
 
 int packmamba_abi_version(void) { return PACKMAMBA_ABI_VERSION; }
@@ -110,6 +131,7 @@ const char* packmamba_status_string(int status) {
         case PACKMAMBA_ERR_ALIGN: return "pointer not 16-byte aligned";
         case PACKMAMBA_ERR_WORKSPACE: return "workspace missing or too small";
         case PACKMAMBA_ERR_LAUNCH: return "kernel launch failed";
+        case PACKMAMBA_ERR_SCRATCH: return "shape needs more than the fixed scratch of the no-allocation entry point";
         default: return "unknown status";
     }
 }
@@ -147,17 +169,10 @@ int packmamba_causal_conv1d_bwd(const void* x, const float* weight, const float*
                                 float* dbias, void* dinitial_x, void* workspace,
                                 size_t workspace_bytes, int64_t batch, int64_t dim, int64_t seqlen,
                                 int32_t width, int32_t dtype, int32_t silu, void* stream) {
-    if (!x || !weight || !position_indices || !dout || !dx || !dweight) return PACKMAMBA_ERR_NULL;
-    if ((bias == nullptr) != (dbias == nullptr)) return PACKMAMBA_ERR_NULL;
-    if ((initial_x == nullptr) != (dinitial_x == nullptr)) return PACKMAMBA_ERR_NULL;
-    if (int e = check_shape(batch, dim, seqlen)) return e;
-    if (int e = check_dtype(dtype)) return e;
-    if (width < 2 || width > 4) return PACKMAMBA_ERR_UNSUPPORTED;
-    if (!aligned16(x) || !aligned16(weight) || !aligned16(bias) || !aligned16(position_indices) ||
-        !aligned16(dout) || !aligned16(dx) || !aligned16(dweight) || !aligned16(dbias) ||
-        !aligned16(workspace) || !aligned16(initial_x) || !aligned16(dfinal_x) ||
-        !aligned16(dinitial_x))
-        return PACKMAMBA_ERR_ALIGN;
+    if (int e = pm::conv1d_bwd_args_status(x, weight, bias, position_indices, initial_x, dout, dfinal_x, dx,
+                                           dweight, dbias, dinitial_x, batch, dim, seqlen, width, dtype))
+        return e;
+    if (!aligned16(workspace)) return PACKMAMBA_ERR_ALIGN;
     const size_t need = packmamba_causal_conv1d_bwd_workspace_size(batch, dim, seqlen, width);
     if (!workspace || workspace_bytes < need) return PACKMAMBA_ERR_WORKSPACE;
     pm::ConvArgs a{};

@@ -26,13 +26,14 @@ def test_exports_every_declared_symbol():
     lib = _lib()
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.packmamba_abi_version() == 5
+    assert lib.packmamba_abi_version() == 6
 
 
 def test_status_strings():
     lib = _lib()
-    for s in range(7):
+    for s in range(8):
         assert lib.packmamba_status_string(s)
+        assert b"unknown" not in lib.packmamba_status_string(s)
     assert b"unknown" in lib.packmamba_status_string(99)
 
 
@@ -112,6 +113,18 @@ def test_argument_errors_before_launch():
     assert cbwd(P, P, None, P, None, P, None, P, P, None, P, P, 1 << 20, 1, 1, 8, 4, 0, 1, None) == 1  # dinitial_x without initial_x
     assert cbwd(P, P, None, P, None, P, None, P, P, None, None, P, 1, 1, 1, 8, 4, 0, 1, None) == 5     # workspace small
     assert cbwd(P, P, None, P, None, P, None, P, P, None, None, None, 1 << 20, 1, 1, 8, 4, 0, 1, None) == 5
+    # the no-allocation variant: the same argument errors, and shapes beyond its fixed scratch
+    na = lib.packmamba_causal_conv1d_bwd_noalloc
+    # x, w, bias, pos, initial_x, dout, dfinal_x, dx, dw, dbias, dinitial_x, batch, dim, seqlen, width, dtype, silu, stream
+    assert na(None, P, None, P, None, P, None, P, P, None, None, 1, 1, 8, 4, 0, 1, None) == 1
+    assert na(P, P, P, P, None, P, None, P, P, None, None, 1, 1, 8, 4, 0, 1, None) == 1       # bias without dbias
+    assert na(P, P, None, P, None, P, None, P, P, None, None, 0, 1, 8, 4, 0, 1, None) == 2
+    assert na(P, P, None, P, None, P, None, P, P, None, None, 1, 1, 8, 5, 0, 1, None) == 3
+    assert na(P, P, None, P, None, P, None, U, P, None, None, 1, 1, 8, 4, 0, 1, None) == 4
+    big = (8, 1 << 17, 8)   # 8 x 131072 x 5 partial floats = 20 MiB > 16 MiB
+    assert lib.packmamba_causal_conv1d_bwd_workspace_size(*big, 4) > (16 << 20)
+    assert na(P, P, None, P, None, P, None, P, P, None, None, *big, 4, 0, 1, None) == 7
+    assert lib.packmamba_causal_conv1d_bwd_workspace_size(8, 4096, 4096, 4) <= (16 << 20)
     fwd = lib.packmamba_selective_scan_fwd
     # u, delta, A, B, C, D, z, delta_bias, softplus, pos, initial_state, out, final_state, states,
     # ws, ws_bytes, batch, dim, seqlen, dstate, dtype, stream
