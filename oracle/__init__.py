@@ -26,7 +26,8 @@ from typing import Dict, Optional
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "liboracle.so")
+# PACKMAMBA_ORACLE_LIB names another build of oracle.c (e.g. a sanitizer build)
+LIB_PATH = os.environ.get("PACKMAMBA_ORACLE_LIB") or os.path.join(_HERE, "liboracle.so")
 SRC_PATH = os.path.join(_HERE, "oracle.c")
 
 _lib = None

@@ -12,7 +12,8 @@ import os
 from typing import Optional
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libpackmamba.so")
+# PACKMAMBA_LIB names another build of the library (e.g. a host-side sanitizer build)
+LIB_PATH = os.environ.get("PACKMAMBA_LIB") or os.path.join(HERE, "libpackmamba.so")
 
 F32, BF16, BF16_F32OUT = 0, 1, 2
 STATE_STRIDE = 128

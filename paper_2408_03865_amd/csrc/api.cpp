@@ -116,6 +116,19 @@ int conv1d_bwd_args_status(const void* x, const float* weight, const float* bias
     return PACKMAMBA_OK;
 }
 
+int conv1d_bwd_noalloc_status(const void* x, const float* weight, const float* bias,
+                              const int32_t* position_indices, const void* initial_x, const void* dout,
+                              const void* dfinal_x, const void* dx, const float* dweight, const float* dbias,
+                              const void* dinitial_x, int64_t batch, int64_t dim, int64_t seqlen, int32_t width,
+                              int32_t dtype) {
+    if (int e = conv1d_bwd_args_status(x, weight, bias, position_indices, initial_x, dout, dfinal_x, dx, dweight,
+                                       dbias, dinitial_x, batch, dim, seqlen, width, dtype))
+        return e;
+    if (packmamba_causal_conv1d_bwd_workspace_size(batch, dim, seqlen, width) > PACKMAMBA_NOALLOC_SCRATCH_BYTES)
+        return PACKMAMBA_ERR_SCRATCH;
+    return PACKMAMBA_OK;
+}
+
 }  // namespace pm
 
 extern "C" {

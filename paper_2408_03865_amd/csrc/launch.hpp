@@ -33,6 +33,13 @@ int conv1d_bwd_args_status(const void* x, const float* weight, const float* bias
                            const void* initial_x, const void* dout, const void* dfinal_x, const void* dx,
                            const float* dweight, const float* dbias, const void* dinitial_x, int64_t batch,
                            int64_t dim, int64_t seqlen, int32_t width, int32_t dtype);
+// The same plus the no-allocation variant's limit: PACKMAMBA_ERR_SCRATCH when the shape's
+// workspace exceeds its fixed scratch.
+int conv1d_bwd_noalloc_status(const void* x, const float* weight, const float* bias,
+                              const int32_t* position_indices, const void* initial_x, const void* dout,
+                              const void* dfinal_x, const void* dx, const float* dweight, const float* dbias,
+                              const void* dinitial_x, int64_t batch, int64_t dim, int64_t seqlen, int32_t width,
+                              int32_t dtype);
 hipError_t launch_conv1d_bwd(const ConvArgs& a, hipStream_t s);
 
 // RMSNorm over the feature axis of (batch, dim, seqlen) activations.

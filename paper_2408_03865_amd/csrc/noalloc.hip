@@ -45,12 +45,11 @@ extern "C" int packmamba_causal_conv1d_bwd_noalloc(
     const void* initial_x, const void* dout, const void* dfinal_x, void* dx, float* dweight,
     float* dbias, void* dinitial_x, int64_t batch, int64_t dim, int64_t seqlen, int32_t width,
     int32_t dtype, int32_t silu, void* stream) {
-    // argument errors first, with nothing enqueued and the scratch not touched
-    if (int e = pm::conv1d_bwd_args_status(x, weight, bias, position_indices, initial_x, dout, dfinal_x, dx,
-                                           dweight, dbias, dinitial_x, batch, dim, seqlen, width, dtype))
+    // argument errors and the scratch limit first, with nothing enqueued and the scratch
+    // not touched
+    if (int e = pm::conv1d_bwd_noalloc_status(x, weight, bias, position_indices, initial_x, dout, dfinal_x, dx,
+                                              dweight, dbias, dinitial_x, batch, dim, seqlen, width, dtype))
         return e;
-    if (packmamba_causal_conv1d_bwd_workspace_size(batch, dim, seqlen, width) > PACKMAMBA_NOALLOC_SCRATCH_BYTES)
-        return PACKMAMBA_ERR_SCRATCH;
     void* ws = nullptr;
     if (int e = scratch_address(&ws)) return e;
     return packmamba_causal_conv1d_bwd(x, weight, bias, position_indices, initial_x, dout, dfinal_x, dx, dweight,
