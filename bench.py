@@ -311,7 +311,7 @@ BLOCK_PHASES = {"norm": "other", "in_proj": "gemm", "conv": "conv", "x_proj": "g
                 "conv_bwd": "conv", "in_proj_bwd": "gemm", "norm_bwd": "other"}
 
 
-def block_bench(args):
+def block_bench(args, d=None):
     """One packed Mamba-1 block (Mamba-1.4B layer: d_model 2048, d_inner 4096, d_state 16,
     dt_rank 128, conv width 4, bf16), forward and backward, on the tokens of the 1.4B
     workload: packed, padded to the longest sequence, and one sequence per call.  The
@@ -326,7 +326,8 @@ def block_bench(args):
     cfg = W.config("2")
     Nb, L, Dn, N = cfg.batch, cfg.seqlen, cfg.dim, cfg.dstate
     dm, R, Wd = 2048, 128, cfg.width
-    d = W.make_inputs(cfg)
+    if d is None:
+        d = W.make_inputs(cfg)
     g = torch.Generator(device=dev).manual_seed(0)
     bf = torch.bfloat16
     rn = lambda *sh: torch.randn(sh, generator=g, device=dev)  # noqa: E731
@@ -405,7 +406,7 @@ def block_bench(args):
         "single": {"calls_per_step": len(seqs), "ms_per_step": round(mss, 4),
                    "packed_speedup": round(mss / ms, 3)},
     }
-    print(json.dumps(res), flush=True)
+    return res
 
 
 def main():
@@ -457,7 +458,7 @@ def main():
         if not os.path.exists(_lib.LIB_PATH):
             import __graft_entry__
             __graft_entry__.build()
-        block_bench(args)
+        print(json.dumps(block_bench(args)), flush=True)
         return
     if not os.path.exists(_lib.LIB_PATH):
         import __graft_entry__
@@ -543,6 +544,11 @@ def main():
             extra[name] = r
             torch.cuda.empty_cache()
         line["workloads"] = extra
+        print("# packed Mamba-1.4B block", file=sys.stderr, flush=True)
+        blk = block_bench(args, d=cpu_d if args.variant == "paper" and args.dtype in (None, "bf16") else None)
+        blk.pop("metric", None)
+        line["block"] = blk
+        torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         print("# cpu baseline (oracle)", file=sys.stderr, flush=True)
         line["cpu_baseline"] = cpu_baseline(cpu_d, cfg, args.cpu_rows)
